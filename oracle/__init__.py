@@ -1,0 +1,213 @@
+"""CPU oracle for the PAIR estimator -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The product library never loads it and
+shares no code with it; see ``pair_oracle.c`` for the paper passages each
+function follows (fp64, explicit edge loops, Philox4x64-10 design draws).
+
+Parity status of each function (what pins it, see ``tests/test_oracle_pins.py``):
+  philox4x64_10     pinned: numpy's independent Philox implementation
+  design_inclusion  pinned: brute-force edge count, inclusion frequencies vs p
+                    (binomial z-test), bit layout of the counter reading
+  pair_grad         pinned: p == 1 reduces to the leave-one-out form (Thm 1);
+                    exhaustive design enumeration reproduces the complete-pair
+                    average (Thm 2); unweighted-bias closed form (Prop 1);
+                    linearity, permutation invariance, zero cases
+  pair_coeffs       pinned: sum_i A~_i s_i equals pair_grad; A~ sums to zero;
+                    p == 1 gives (r_i - mean r)/(G - 1)
+  audit             pinned: exact design covariance trace (Prop 1) by
+                    enumeration; Gram-matrix identity for every replicate;
+                    bias^2 ~ MSE/R statistics; p == 1 gives zero MSE
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "pair_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+F32 = 0
+BF16 = 1
+
+ERRORS = {
+    0: "ok",
+    -1: "invalid argument",
+    -2: "unknown dtype",
+    -3: "observed edge with rho outside (0, 1]",
+    -4: "continuation probability outside (0, 1]",
+    -5: "prompt with fewer than two candidates",
+}
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def build(force: bool = True) -> str:
+    """Compile pair_oracle.c into liboracle.so with gcc (fp64, no contraction)."""
+    if force or not os.path.exists(_LIB):
+        cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
+               "-fPIC", "-shared", "-Wall", "-Wextra", "-o", _LIB + ".tmp", _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i64, i32, u64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
+        lib.orc_philox4x64_10.argtypes = [P, P, P]
+        lib.orc_philox4x64_10.restype = None
+        lib.orc_draw_indicator.argtypes = [u64, i64, i64, i64, ctypes.c_float]
+        lib.orc_draw_indicator.restype = ctypes.c_int
+        lib.orc_design_inclusion.argtypes = [i64, P, i32, P, u64, i64, i64, P, P, P, P, P]
+        lib.orc_design_inclusion.restype = ctypes.c_int
+        lib.orc_pair_grad.argtypes = [i64, P, i32, i64, P, ctypes.c_int, i64, P, P, P, P, P]
+        lib.orc_pair_grad.restype = ctypes.c_int
+        lib.orc_pair_coeffs.argtypes = [i64, P, i32, P, P, P, P, P]
+        lib.orc_pair_coeffs.restype = ctypes.c_int
+        lib.orc_audit.argtypes = [i64, P, i32, i64, P, ctypes.c_int, i64, P, P, P, u64, i64, i64,
+                                  P, P, P, P, P]
+        lib.orc_audit.restype = ctypes.c_int
+        lib.orc_num_threads.argtypes = []
+        lib.orc_num_threads.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(rc):
+    if rc != 0:
+        raise OracleError(f"oracle error {rc}: {ERRORS.get(rc, '?')}")
+
+
+def _scores_arg(scores):
+    """Return (array, dtype code, ld).  bf16 scores are passed as their uint16 bits."""
+    if scores.dtype == np.float32:
+        code = F32
+    elif scores.dtype == np.uint16:
+        code = BF16
+    else:
+        raise TypeError("scores must be float32 or uint16 (bf16 bit patterns)")
+    if scores.ndim != 2 or scores.strides[1] != scores.itemsize:
+        raise ValueError("scores must be a row-major 2-D array")
+    ld = scores.strides[0] // scores.itemsize
+    return scores, code, ld
+
+
+def _offsets(offsets):
+    return np.ascontiguousarray(offsets, dtype=np.int64)
+
+
+def num_threads() -> int:
+    return _load().orc_num_threads()
+
+
+def philox4x64_10(ctr, key):
+    lib = _load()
+    c = np.ascontiguousarray(ctr, dtype=np.uint64)
+    k = np.ascontiguousarray(key, dtype=np.uint64)
+    out = np.zeros(4, dtype=np.uint64)
+    lib.orc_philox4x64_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def draw_indicator(seed, r, b, i, p):
+    return _load().orc_draw_indicator(seed, r, b, i, float(np.float32(p)))
+
+
+def design_inclusion(offsets, p, seed, rep0, R, gmax, prompt_id=None, want_pi=True):
+    """Returns dict(mask[R][nv] u8, pi[B][gmax][gmax] f32, edge_count[R][B], completed[R][B])."""
+    lib = _load()
+    off = _offsets(offsets)
+    B = off.size - 1
+    nv = int(off[-1])
+    p = np.ascontiguousarray(p, dtype=np.float32)
+    mask = np.zeros((R, nv), dtype=np.uint8)
+    pi = np.zeros((B, gmax, gmax), dtype=np.float32) if want_pi else None
+    ec = np.zeros((R, B), dtype=np.int32)
+    comp = np.zeros((R, B), dtype=np.int32)
+    pid = None if prompt_id is None else np.ascontiguousarray(prompt_id, dtype=np.int64)
+    _check(lib.orc_design_inclusion(B, _ptr(off), gmax, _ptr(p), seed, rep0, R, _ptr(pid),
+                                    _ptr(mask), _ptr(pi), _ptr(ec), _ptr(comp)))
+    return {"mask": mask, "pi": pi, "edge_count": ec, "completed": comp}
+
+
+def pair_grad(offsets, scores, rewards, mask=None, pi=None, gmax=None):
+    """Eq. (pair-ht) per prompt in fp64: returns (out[B][D] float64, edge_count[B])."""
+    lib = _load()
+    off = _offsets(offsets)
+    B = off.size - 1
+    s, code, ld = _scores_arg(scores)
+    D = s.shape[1]
+    r = np.ascontiguousarray(rewards, dtype=np.float32)
+    m = None if mask is None else np.ascontiguousarray(mask, dtype=np.uint8)
+    if pi is not None:
+        pi = np.ascontiguousarray(pi, dtype=np.float32)
+        gmax = pi.shape[-1]
+    if gmax is None:
+        gmax = int(np.max(np.diff(off)))
+    out = np.zeros((B, D), dtype=np.float64)
+    ec = np.zeros(B, dtype=np.int32)
+    _check(lib.orc_pair_grad(B, _ptr(off), gmax, D, _ptr(s), code, ld, _ptr(r), _ptr(m), _ptr(pi),
+                             _ptr(out), _ptr(ec)))
+    return out, ec
+
+
+def pair_coeffs(offsets, rewards, mask=None, pi=None, gmax=None):
+    """Eq. (pair-advantage) in Algorithm 1's edge order: returns (coeff[nv] f64, edge_count[B])."""
+    lib = _load()
+    off = _offsets(offsets)
+    B = off.size - 1
+    r = np.ascontiguousarray(rewards, dtype=np.float32)
+    m = None if mask is None else np.ascontiguousarray(mask, dtype=np.uint8)
+    if pi is not None:
+        pi = np.ascontiguousarray(pi, dtype=np.float32)
+        gmax = pi.shape[-1]
+    if gmax is None:
+        gmax = int(np.max(np.diff(off)))
+    coeff = np.zeros(int(off[-1]), dtype=np.float64)
+    ec = np.zeros(B, dtype=np.int32)
+    _check(lib.orc_pair_coeffs(B, _ptr(off), gmax, _ptr(r), _ptr(m), _ptr(pi), _ptr(coeff), _ptr(ec)))
+    return coeff, ec
+
+
+def audit(offsets, scores, rewards, p, seed, rep0, R, pi_w=None, gmax=None, prompt_id=None,
+          want_reps=True):
+    """Frozen-population audit: returns dict(mse[B], bias_norm[B], rep_sqerr[B][R], edge_count[B][R])."""
+    lib = _load()
+    off = _offsets(offsets)
+    B = off.size - 1
+    s, code, ld = _scores_arg(scores)
+    D = s.shape[1]
+    r = np.ascontiguousarray(rewards, dtype=np.float32)
+    pp = np.ascontiguousarray(p, dtype=np.float32)
+    if pi_w is not None:
+        pi_w = np.ascontiguousarray(pi_w, dtype=np.float32)
+        gmax = pi_w.shape[-1]
+    if gmax is None:
+        gmax = int(np.max(np.diff(off)))
+    pid = None if prompt_id is None else np.ascontiguousarray(prompt_id, dtype=np.int64)
+    mse = np.zeros(B, dtype=np.float64)
+    bias = np.zeros(B, dtype=np.float64)
+    reps = np.zeros((B, R), dtype=np.float64) if want_reps else None
+    ec = np.zeros((B, R), dtype=np.int32) if want_reps else None
+    _check(lib.orc_audit(B, _ptr(off), gmax, D, _ptr(s), code, ld, _ptr(r), _ptr(pp), _ptr(pi_w),
+                         seed, rep0, R, _ptr(pid), _ptr(mse), _ptr(bias), _ptr(reps), _ptr(ec)))
+    return {"mse": mse, "bias_norm": bias, "rep_sqerr": reps, "edge_count": ec}

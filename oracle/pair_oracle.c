@@ -1,0 +1,369 @@
+/*
+ * pair_oracle.c -- plain, slow, obviously correct CPU reference for the PAIR
+ * pair-inclusion-weighted gradient estimator and its frozen-population audit.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may call, link or
+ * load this file; only the test-suite, the smoke check and the bench's CPU
+ * baseline leg use it.  It shares no code, header, table or constant with the
+ * HIP library: everything below is written from the paper's definitions.
+ *
+ * Arithmetic is IEEE fp64, built with -ffp-contract=off and without fast-math.
+ * Inputs are the exact fp32 / bf16 values the GPU sees, widened exactly.
+ *
+ * Paper sections followed:
+ *   - Sec. 2.1, Eq. (loo)            leave-one-out gradient (used only by pins)
+ *   - Sec. 2.2, Eq. (pair-kernel)    h_ij = 1/2 (r_i - r_j)(s_i - s_j)
+ *   - Sec. 2.2, Eq. (pair-average)   complete-pair average, M = C(G,2)
+ *   - Sec. 2.3                       adaptive continuation: J_i, I_ij = J_i J_j,
+ *                                    rho_ij = P(J_i J_j = 1), independent
+ *                                    Bernoulli => rho_ij = pi_i pi_j, logged
+ *   - Sec. 3.5, Eq. (pair-ht)        induced-edge Horvitz-Thompson estimator
+ *   - Sec. 3.5, Eq. (pair-advantage) sequence advantages A~_i
+ *   - Algorithm 1 (pair-corrected update): enumerate observed edges and
+ *                                    accumulate h_ij / rho_ij into A~_i, A~_j
+ *   - App. B "At least two completed vertices": a draw with fewer than two
+ *                                    completed vertices contributes zero
+ *   - Sec. 5.2 frozen-policy audit and App. D metrics: MSE = E||g^ - g_full||^2,
+ *                                    bias = || mean_r g^_r - g_full ||
+ *
+ * Random design draws.  The paper only requires fresh randomisation for the
+ * continuation indicators.  This oracle fixes one counter-based generator, the
+ * published Philox4x64 with 10 rounds (Salmon, Moraes, Dror, Shaw, "Parallel
+ * random numbers: as easy as 1, 2, 3", SC'11), and the reading:
+ *   key     = (seed, 0)
+ *   counter = (replicate r, prompt id b, i >> 2, 0)
+ *   u_i     = top 32 bits of output word (i & 3)
+ *   J_i     = [ u_i < floor(p_i * 2^32) ]     (p_i >= 1 always includes)
+ * so that P(J_i = 1) = floor(p_i 2^32) / 2^32, which equals p_i exactly for
+ * every fp32 p_i >= 2^-9.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_OK 0
+#define ORC_EINVAL (-1)   /* malformed sizes / offsets / pointers            */
+#define ORC_EDTYPE (-2)   /* unknown score dtype                              */
+#define ORC_ERHO (-3)     /* observed edge with rho outside (0, 1]            */
+#define ORC_EP (-4)       /* continuation probability outside (0, 1]          */
+#define ORC_EGROUP (-5)   /* a prompt with fewer than two candidates          */
+
+#define ORC_F32 0
+#define ORC_BF16 1
+
+/* ------------------------------------------------------------------------ */
+/* Philox4x64-10, written from the SC'11 description: each round multiplies  */
+/* words 0 and 2 by the two round multipliers, takes the 128-bit products'   */
+/* high and low halves, and xors the high halves with the other two words    */
+/* and the key; the key is bumped by the two Weyl constants between rounds.  */
+/* ------------------------------------------------------------------------ */
+static void mul64_full(uint64_t a, uint64_t b, uint64_t* hi, uint64_t* lo) {
+    unsigned __int128 prod = (unsigned __int128)a * (unsigned __int128)b;
+    *hi = (uint64_t)(prod >> 64);
+    *lo = (uint64_t)prod;
+}
+
+void orc_philox4x64_10(const uint64_t ctr_in[4], const uint64_t key_in[2], uint64_t out[4]) {
+    const uint64_t mult0 = 0xD2E7470EE14C6C93ULL, mult1 = 0xCA5A826395121157ULL;
+    const uint64_t weyl0 = 0x9E3779B97F4A7C15ULL, weyl1 = 0xBB67AE8584CAA73BULL;
+    uint64_t x0 = ctr_in[0], x1 = ctr_in[1], x2 = ctr_in[2], x3 = ctr_in[3];
+    uint64_t k0 = key_in[0], k1 = key_in[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k0 += weyl0;
+            k1 += weyl1;
+        }
+        uint64_t hi0, lo0, hi1, lo1;
+        mul64_full(mult0, x0, &hi0, &lo0);
+        mul64_full(mult1, x2, &hi1, &lo1);
+        uint64_t y0 = hi1 ^ x1 ^ k0;
+        uint64_t y1 = lo1;
+        uint64_t y2 = hi0 ^ x3 ^ k1;
+        uint64_t y3 = lo0;
+        x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+    }
+    out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
+}
+
+/* Continuation indicator J_i for vertex i of prompt id b in replicate r. */
+int orc_draw_indicator(uint64_t seed, int64_t r, int64_t b, int64_t i, float p) {
+    uint64_t ctr[4] = {(uint64_t)r, (uint64_t)b, (uint64_t)(i >> 2), 0};
+    uint64_t key[2] = {seed, 0};
+    uint64_t w[4];
+    orc_philox4x64_10(ctr, key, w);
+    uint64_t u = w[i & 3] >> 32;
+    if (p >= 1.0f) return 1;
+    uint64_t thr = (uint64_t)ldexp((double)p, 32); /* exact: p*2^32 < 2^32 */
+    return u < thr ? 1 : 0;
+}
+
+/* Score element s[v][d] widened exactly to fp64. */
+static double score_at(const void* scores, int dtype, int64_t ld, int64_t v, int64_t d) {
+    if (dtype == ORC_F32) {
+        return (double)((const float*)scores)[v * ld + d];
+    }
+    uint16_t h = ((const uint16_t*)scores)[v * ld + d];
+    uint32_t bits = ((uint32_t)h) << 16; /* bf16 is the top half of an fp32 */
+    float f;
+    memcpy(&f, &bits, sizeof f);
+    return (double)f;
+}
+
+static int check_offsets(int64_t B, const int64_t* offsets, int32_t gmax) {
+    if (B < 1 || offsets == NULL || offsets[0] != 0) return ORC_EINVAL;
+    for (int64_t b = 0; b < B; ++b) {
+        int64_t g = offsets[b + 1] - offsets[b];
+        if (g < 2) return ORC_EGROUP;
+        if (gmax > 0 && g > gmax) return ORC_EINVAL;
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Design draw (Sec. 2.3): independent Bernoulli continuation with logged    */
+/* joint inclusion probabilities rho_ij = pi_i pi_j.                         */
+/*   mask[r][v]        J for vertex v in replicate rep0 + r                  */
+/*   pi[b][i][j]       fp32 rho_ij (i != j), pi_i on the diagonal, 0 beyond  */
+/*                     G_b; rounded once from the exact fp64 product         */
+/*   edge_count[r][b]  K_E = number of i < j with J_i = J_j = 1 (brute force) */
+/*   completed[r][b]   number of completed vertices                          */
+/* prompt_id: RNG prompt index of each prompt (NULL => 0..B-1).              */
+/* ------------------------------------------------------------------------ */
+int orc_design_inclusion(int64_t B, const int64_t* offsets, int32_t gmax, const float* p,
+                         uint64_t seed, int64_t rep0, int64_t R, const int64_t* prompt_id,
+                         uint8_t* mask, float* pi, int32_t* edge_count, int32_t* completed) {
+    int st = check_offsets(B, offsets, gmax);
+    if (st) return st;
+    if (R < 0 || p == NULL) return ORC_EINVAL;
+    int64_t nv = offsets[B];
+    for (int64_t v = 0; v < nv; ++v)
+        if (!(p[v] > 0.0f && p[v] <= 1.0f)) return ORC_EP;
+
+    if (pi != NULL) {
+        for (int64_t b = 0; b < B; ++b) {
+            int64_t o = offsets[b], g = offsets[b + 1] - offsets[b];
+            float* blk = pi + b * (int64_t)gmax * gmax;
+            for (int64_t i = 0; i < gmax; ++i)
+                for (int64_t j = 0; j < gmax; ++j) {
+                    float val = 0.0f;
+                    if (i < g && j < g) {
+                        if (i == j)
+                            val = p[o + i];
+                        else
+                            val = (float)((double)p[o + i] * (double)p[o + j]);
+                    }
+                    blk[i * gmax + j] = val;
+                }
+        }
+    }
+    int64_t gcap = 0;
+    for (int64_t b = 0; b < B; ++b)
+        if (offsets[b + 1] - offsets[b] > gcap) gcap = offsets[b + 1] - offsets[b];
+    int* J = (int*)malloc((size_t)gcap * sizeof(int));
+    if (J == NULL) return ORC_EINVAL;
+    for (int64_t r = 0; r < R; ++r) {
+        for (int64_t b = 0; b < B; ++b) {
+            int64_t o = offsets[b], g = offsets[b + 1] - offsets[b];
+            int64_t bid = prompt_id ? prompt_id[b] : b;
+            int32_t k = 0, ke = 0;
+            for (int64_t i = 0; i < g; ++i) {
+                J[i] = orc_draw_indicator(seed, rep0 + r, bid, i, p[o + i]);
+                if (mask) mask[r * nv + o + i] = (uint8_t)J[i];
+                k += J[i];
+            }
+            for (int64_t i = 0; i < g; ++i) /* brute-force count of induced edges */
+                for (int64_t j = i + 1; j < g; ++j)
+                    if (J[i] && J[j]) ++ke;
+            if (edge_count) edge_count[r * B + b] = ke;
+            if (completed) completed[r * B + b] = k;
+        }
+    }
+    free(J);
+    return ORC_OK;
+}
+
+/* rho_ij read from the upper triangle of one prompt's dense gmax x gmax block. */
+static double rho_of(const float* blk, int32_t gmax, int64_t i, int64_t j) {
+    int64_t lo = i < j ? i : j, hi = i < j ? j : i;
+    return (double)blk[lo * gmax + hi];
+}
+
+/* ------------------------------------------------------------------------ */
+/* Induced-edge HT estimator, Eq. (pair-ht), one prompt, columns [0, D):     */
+/*   g = (1/M) sum_{i<j} (J_i J_j / rho_ij) h_ij,   M = G (G - 1) / 2.       */
+/* mask == NULL means every vertex completed; rho_blk == NULL means rho == 1 */
+/* (together: the complete-pair average of Eq. (pair-average)).             */
+/* ------------------------------------------------------------------------ */
+static int ht_estimate_one(int64_t o, int64_t g, int64_t D, const void* scores, int dtype,
+                           int64_t ld, const float* rewards, const uint8_t* mask,
+                           const float* rho_blk, int32_t gmax, double* out, int32_t* edges) {
+    const double M = (double)g * (double)(g - 1) / 2.0;
+    int32_t ke = 0;
+    for (int64_t d = 0; d < D; ++d) out[d] = 0.0;
+    for (int64_t i = 0; i < g; ++i) {
+        for (int64_t j = i + 1; j < g; ++j) {
+            int Ji = mask ? mask[o + i] != 0 : 1;
+            int Jj = mask ? mask[o + j] != 0 : 1;
+            if (!(Ji && Jj)) continue; /* I_ij = 0: the edge is not observed */
+            ++ke;
+            double rho = rho_blk ? rho_of(rho_blk, gmax, i, j) : 1.0;
+            if (!(rho > 0.0 && rho <= 1.0)) return ORC_ERHO;
+            double ri = (double)rewards[o + i], rj = (double)rewards[o + j];
+            for (int64_t d = 0; d < D; ++d) {
+                double si = score_at(scores, dtype, ld, o + i, d);
+                double sj = score_at(scores, dtype, ld, o + j, d);
+                double h = 0.5 * (ri - rj) * (si - sj); /* Eq. (pair-kernel) */
+                out[d] += h / rho;
+            }
+        }
+    }
+    for (int64_t d = 0; d < D; ++d) out[d] /= M;
+    if (edges) *edges = ke;
+    return ORC_OK;
+}
+
+/* Batched Eq. (pair-ht): out[b][d] for every prompt; edge_count[b] = K_E. */
+int orc_pair_grad(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D, const void* scores,
+                  int dtype, int64_t ld, const float* rewards, const uint8_t* mask, const float* pi,
+                  double* out, int32_t* edge_count) {
+    int st = check_offsets(B, offsets, gmax);
+    if (st) return st;
+    if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_EDTYPE;
+    if (D < 0 || ld < D || scores == NULL || rewards == NULL || out == NULL) return ORC_EINVAL;
+    int err = ORC_OK;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        int64_t o = offsets[b], g = offsets[b + 1] - offsets[b];
+        const float* blk = pi ? pi + b * (int64_t)gmax * gmax : NULL;
+        int s = ht_estimate_one(o, g, D, scores, dtype, ld, rewards, mask, blk, gmax, out + b * D,
+                                edge_count ? edge_count + b : NULL);
+        if (s) {
+#pragma omp critical
+            err = s;
+        }
+    }
+    return err;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sequence advantages, Eq. (pair-advantage), in the order of Algorithm 1:   */
+/* for every observed edge (i, j), i < j, the edge term h_ij / rho_ij puts   */
+/* (r_i - r_j) / (2 rho_ij) on s_i and its negative on s_j; divide by M.     */
+/* ------------------------------------------------------------------------ */
+int orc_pair_coeffs(int64_t B, const int64_t* offsets, int32_t gmax, const float* rewards,
+                    const uint8_t* mask, const float* pi, double* coeff, int32_t* edge_count) {
+    int st = check_offsets(B, offsets, gmax);
+    if (st) return st;
+    if (rewards == NULL || coeff == NULL) return ORC_EINVAL;
+    for (int64_t b = 0; b < B; ++b) {
+        int64_t o = offsets[b], g = offsets[b + 1] - offsets[b];
+        double M = (double)g * (double)(g - 1) / 2.0;
+        int32_t ke = 0;
+        for (int64_t i = 0; i < g; ++i) coeff[o + i] = 0.0;
+        for (int64_t i = 0; i < g; ++i) {
+            for (int64_t j = i + 1; j < g; ++j) {
+                int Ji = mask ? mask[o + i] != 0 : 1;
+                int Jj = mask ? mask[o + j] != 0 : 1;
+                if (!(Ji && Jj)) continue;
+                ++ke;
+                double rho = pi ? rho_of(pi + b * (int64_t)gmax * gmax, gmax, i, j) : 1.0;
+                if (!(rho > 0.0 && rho <= 1.0)) return ORC_ERHO;
+                double t = ((double)rewards[o + i] - (double)rewards[o + j]) / (2.0 * rho);
+                coeff[o + i] += t;
+                coeff[o + j] -= t;
+            }
+        }
+        for (int64_t i = 0; i < g; ++i) coeff[o + i] /= M;
+        if (edge_count) edge_count[b] = ke;
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Frozen-population audit (Sec. 5.2, App. D).  For each prompt:             */
+/*   target  t   = complete-pair average, Eq. (pair-average)                 */
+/*   for r in [rep0, rep0 + R): draw J^(r) as orc_design_inclusion does,     */
+/*       g_r = Eq. (pair-ht) with weights 1/rho, rho = pi_w[b][i][j] when    */
+/*       pi_w is given, otherwise the logged fl32(p_i p_j);                  */
+/*       e_r = || g_r - t ||^2                                               */
+/*   mse  = (1/R) sum_r e_r ;  bias = || (1/R) sum_r g_r - t ||              */
+/* rep_sqerr[b][R] and edge_count[b][R] are optional per-replicate outputs. */
+/* ------------------------------------------------------------------------ */
+int orc_audit(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D, const void* scores,
+              int dtype, int64_t ld, const float* rewards, const float* p, const float* pi_w,
+              uint64_t seed, int64_t rep0, int64_t R, const int64_t* prompt_id, double* mse,
+              double* bias_norm, double* rep_sqerr, int32_t* edge_count) {
+    int st = check_offsets(B, offsets, gmax);
+    if (st) return st;
+    if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_EDTYPE;
+    if (D < 1 || ld < D || R < 1 || scores == NULL || rewards == NULL || p == NULL) return ORC_EINVAL;
+    int64_t nv = offsets[B];
+    for (int64_t v = 0; v < nv; ++v)
+        if (!(p[v] > 0.0f && p[v] <= 1.0f)) return ORC_EP;
+    int err = ORC_OK;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        int64_t o = offsets[b], g = offsets[b + 1] - offsets[b];
+        int64_t bid = prompt_id ? prompt_id[b] : b;
+        double* t = (double*)calloc((size_t)D, sizeof(double));
+        double* gr = (double*)calloc((size_t)D, sizeof(double));
+        double* gsum = (double*)calloc((size_t)D, sizeof(double));
+        uint8_t* m = (uint8_t*)calloc((size_t)nv, 1);
+        float* own = (float*)calloc((size_t)gmax * gmax, sizeof(float));
+        int s = ORC_OK;
+        if (!t || !gr || !gsum || !m || !own) s = ORC_EINVAL;
+        /* weights' rho: the caller's block, or the logged fl32(p_i p_j) */
+        const float* blk = own;
+        if (pi_w) {
+            blk = pi_w + b * (int64_t)gmax * gmax;
+        } else {
+            for (int64_t i = 0; s == ORC_OK && i < g; ++i)
+                for (int64_t j = 0; j < g; ++j)
+                    if (i != j) own[i * gmax + j] = (float)((double)p[o + i] * (double)p[o + j]);
+        }
+        if (s == ORC_OK)
+            s = ht_estimate_one(o, g, D, scores, dtype, ld, rewards, NULL, NULL, gmax, t, NULL);
+        double esum = 0.0;
+        for (int64_t r = 0; s == ORC_OK && r < R; ++r) {
+            for (int64_t i = 0; i < g; ++i)
+                m[o + i] = (uint8_t)orc_draw_indicator(seed, rep0 + r, bid, i, p[o + i]);
+            int32_t ke = 0;
+            s = ht_estimate_one(o, g, D, scores, dtype, ld, rewards, m, blk, gmax, gr, &ke);
+            if (s) break;
+            double e = 0.0;
+            for (int64_t d = 0; d < D; ++d) {
+                double dev = gr[d] - t[d];
+                e += dev * dev;
+                gsum[d] += gr[d];
+            }
+            esum += e;
+            if (rep_sqerr) rep_sqerr[b * R + r] = e;
+            if (edge_count) edge_count[b * R + r] = ke;
+        }
+        if (s == ORC_OK) {
+            double bb = 0.0;
+            for (int64_t d = 0; d < D; ++d) {
+                double dev = gsum[d] / (double)R - t[d];
+                bb += dev * dev;
+            }
+            if (mse) mse[b] = esum / (double)R;
+            if (bias_norm) bias_norm[b] = sqrt(bb);
+        } else {
+#pragma omp critical
+            err = s;
+        }
+        free(t); free(gr); free(gsum); free(m); free(own);
+    }
+    return err;
+}
+
+/* Number of OpenMP threads the parallel loops above will use. */
+int orc_num_threads(void) {
+#ifdef _OPENMP
+    extern int omp_get_max_threads(void);
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
