@@ -1,0 +1,283 @@
+#!/usr/bin/env python3
+"""Benchmark of the PAIR hot path on one MI355X.
+
+One step = one pass of every stage of the hot path over resident synthetic
+inputs:
+  gradient chain on workload b128 (B=128 prompts, G=16, D=2^20 bf16 scores):
+      pair_design_inclusion -> pair_edge_coeffs -> pair_weighted_grad
+  estimator audit on workload audit (B=256, G=16, D=65536 bf16, R=4096):
+      pair_audit (replicate coefficients, matrix-core contraction with the
+      squared-norm epilogue, fp64 reductions)
+
+Prints ONE JSON line.  `value` is the gradient chain's throughput in GB/s of
+algorithmic bytes (score rows with a nonzero coefficient, the coefficients,
+and the fp32 output), i.e. bytes that must cross HBM, over the chain's event
+time.  The audit is reported in replicate-estimates/s and TFLOP/s (2*G*D flop
+per replicate estimate) in the "audit" object.  "roofline" is for the
+weighted-gradient kernel (the kernel `value` measures), timed with HIP events
+on the stream it is launched on.
+
+Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = ("weighted-grad score GB/s (% HBM peak); "
+          "audit replicate-estimates/s (% MFMA peak)")
+HBM_PEAK_GBPS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+COUNTERS = os.path.join(ROOT, "profiles", "counters.json")
+
+
+def _log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def _source_sha(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2608_11368_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def _traffic(kernel, sources):
+    """HBM bytes per launch from committed rocprofv3 counter runs, or None when
+    the kernel's source changed since the counters were taken."""
+    try:
+        with open(COUNTERS) as f:
+            rec = json.load(f).get(kernel)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_sha") != _source_sha(*sources):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(meta, w, scores_dev, meta_a, wa, scores_a_dev, budget_s=12.0):
+    """The CPU oracle as it stands, timed on the host cores on bounded samples:
+    the gradient chain on a column slice of the b128 scores (all prompts), and
+    the audit on one prompt for a replicate window.  Returns a dict."""
+    import numpy as np
+
+    import oracle
+    from tests.gpu_util import scores_to_host
+
+    cores = oracle.num_threads()
+    # gradient: grow the column slice until the run is long enough
+    cols = 2048
+    while True:
+        s_host = scores_to_host(scores_dev[:, :cols])
+        t0 = time.perf_counter()
+        d = oracle.design_inclusion(meta.offsets, meta.p, w.design_seed, 0, 1, meta.gmax)
+        est, _ = oracle.pair_grad(meta.offsets, s_host, meta.rewards, d["mask"][0], d["pi"])
+        dt = time.perf_counter() - t0
+        coeff, _ = oracle.pair_coeffs(meta.offsets, meta.rewards, d["mask"][0], d["pi"])
+        if dt >= budget_s / 2 or cols >= w.D:
+            break
+        cols = min(w.D, cols * max(2, int(budget_s / 2 / max(dt, 1e-3))))
+    nz_rows = int(np.count_nonzero(coeff))
+    grad_bytes = nz_rows * cols * 2 + meta.nv * 4 + meta.B * cols * 4
+    # audit: one prompt, growing replicate window
+    b = 0
+    o0, o1 = meta_a.offsets[b], meta_a.offsets[b + 1]
+    sa = scores_to_host(scores_a_dev[o0:o1])
+    reps = 8
+    while True:
+        t0 = time.perf_counter()
+        oracle.audit(np.array([0, o1 - o0]), sa, meta_a.rewards[o0:o1], meta_a.p[o0:o1],
+                     wa.design_seed, 0, reps, prompt_id=[b], want_reps=False)
+        da = time.perf_counter() - t0
+        if da >= budget_s / 2 or reps >= wa.R:
+            break
+        reps = min(wa.R, reps * max(2, int(budget_s / 2 / max(da, 1e-3))))
+    return {
+        "value": grad_bytes / dt / 1e9,
+        "unit": "GB/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": (f"gradient chain (design draw + explicit-edge fp64 estimator) on all "
+                   f"{meta.B} prompts x first {cols} of {w.D} columns: {dt:.2f} s; "
+                   f"audit on prompt {b}, {reps} replicates x D={wa.D}: {da:.2f} s"),
+        "audit_value": reps / da,
+        "audit_unit": "replicate-estimates/s",
+        "seconds": dt + da,
+    }
+
+
+def copy_calibration(gib=1.0, reps=5):
+    """Plain device copy of known size, for scaling rocprofv3 FETCH/WRITE counters."""
+    import torch
+
+    n = int(gib * (1 << 30)) // 2
+    src = torch.empty(n, dtype=torch.bfloat16, device="cuda:0").normal_()
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n * 2, "reps": reps}), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one MI355X: this build runs on a single GPU "
+              "(no collectives); run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2608_11368_amd as pair
+    import workloads as wl
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.Stream(device=dev)
+
+    # ---- gradient-chain inputs (b128) ----
+    w = wl.WORKLOADS["b128"]
+    meta = wl.host_meta(w)
+    B, nv, G, D = meta.B, meta.nv, meta.gmax, w.D
+    off = torch.from_numpy(meta.offsets).to(dev)
+    rew = torch.from_numpy(meta.rewards).to(dev)
+    p = torch.from_numpy(meta.p).to(dev)
+    _log(f"[bench] generating b128 scores {nv}x{D} bf16")
+    scores = wl.device_scores(w, nv, dev)
+    mask = torch.empty((1, nv), dtype=torch.uint8, device=dev)
+    pi = torch.empty((B, G, G), dtype=torch.float32, device=dev)
+    ec = torch.empty((1, B), dtype=torch.int32, device=dev)
+    comp = torch.empty((1, B), dtype=torch.int32, device=dev)
+    coeff = torch.empty(nv, dtype=torch.float32, device=dev)
+    out = torch.empty((B, D), dtype=torch.float32, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    # ---- audit inputs ----
+    wa = wl.WORKLOADS["audit"]
+    meta_a = wl.host_meta(wa)
+    Ba, nva, Ga, Da, R = meta_a.B, meta_a.nv, meta_a.gmax, wa.D, wa.R
+    off_a = torch.from_numpy(meta_a.offsets).to(dev)
+    rew_a = torch.from_numpy(meta_a.rewards).to(dev)
+    p_a = torch.from_numpy(meta_a.p).to(dev)
+    _log(f"[bench] generating audit scores {nva}x{Da} bf16")
+    scores_a = wl.device_scores(wa, nva, dev)
+    ws = torch.empty(pair.pair_audit_workspace_bytes(Ba, Ga, Da, R), dtype=torch.uint8, device=dev)
+    mse = torch.empty(Ba, dtype=torch.float64, device=dev)
+    bias = torch.empty(Ba, dtype=torch.float64, device=dev)
+    reps = torch.empty((Ba, R), dtype=torch.float32, device=dev)
+    ec_a = torch.empty((Ba, R), dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+
+    def step(ev):
+        ev[0].record(stream)
+        pair.pair_design_inclusion(B, nv, G, off, p, w.design_seed, 0, 1, mask, pi, ec, comp,
+                                   status, stream)
+        ev[1].record(stream)
+        pair.pair_edge_coeffs(B, nv, G, off, rew, mask[0], pi, coeff, None, status, stream)
+        ev[2].record(stream)
+        pair.pair_weighted_grad(B, nv, off, scores, coeff, out, status, stream)
+        ev[3].record(stream)
+        pair.pair_audit(Ba, nva, Ga, off_a, scores_a, rew_a, p_a, None, wa.design_seed, 0, R, mse,
+                        bias, reps, ec_a, ws, status, stream)
+        ev[4].record(stream)
+
+    def events():
+        return [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            step(events())
+        torch.cuda.synchronize()
+        if int(status.item()) != 0:
+            raise RuntimeError(f"device status {int(status.item())}")
+        evs = [events() for _ in range(args.steps)]
+        _log(f"[bench] timing {args.steps} steps")
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(args.steps):
+            step(evs[k])
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+
+    def part(a, b):
+        return float(np.mean([e[a].elapsed_time(e[b]) for e in evs]))   # ms
+
+    ms_design, ms_coeffs, ms_wgrad, ms_audit = part(0, 1), part(1, 2), part(2, 3), part(3, 4)
+    ms_chain = ms_design + ms_coeffs + ms_wgrad
+    ms_step = (t1 - t0) * 1e3 / args.steps
+
+    nz_rows = int(torch.count_nonzero(coeff).item())
+    bytes_wgrad = nz_rows * D * 2 + nv * 4 + (B + 1) * 8 + B * D * 4
+    bytes_dense = nv * D * 2 + nv * 4 + (B + 1) * 8 + B * D * 4
+    gbps_chain = bytes_wgrad / (ms_chain * 1e-3) / 1e9
+    gbps_wgrad = bytes_wgrad / (ms_wgrad * 1e-3) / 1e9
+    flops_audit = 2.0 * Ba * R * Ga * Da
+    tflops_audit = flops_audit / (ms_audit * 1e-3) / 1e12
+
+    roof_w = {"kernel": "wgrad_kernel<bf16> (pair_weighted_grad)", "bound": "hbm",
+              "achieved": round(gbps_wgrad, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+              "frac": round(gbps_wgrad / HBM_PEAK_GBPS, 4),
+              "traffic": _traffic("wgrad_b128", ["wgrad.hip", "common.hpp"]),
+              "ms": round(ms_wgrad, 4), "algorithmic_bytes": bytes_wgrad}
+    roof_a = {"kernel": "pair_audit (coeffs + mean + mfma + finalize)", "bound": "mfma",
+              "achieved": round(tflops_audit, 1), "peak": BF16_MFMA_PEAK_TFLOPS,
+              "unit": "TFLOP/s", "frac": round(tflops_audit / BF16_MFMA_PEAK_TFLOPS, 4),
+              "traffic": _traffic("audit_b256", ["audit.hip", "common.hpp"]),
+              "ms": round(ms_audit, 4), "flops": flops_audit}
+
+    result = {
+        "metric": METRIC,
+        "value": round(gbps_chain, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "accumulate": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "b128 gradient chain + audit",
+            "grad": {"B": B, "G": G, "D": D, "scores": "bf16 N(0,1/D)", "nv": nv,
+                     "rows_nonzero": nz_rows},
+            "audit": {"B": Ba, "G": Ga, "D": Da, "R": R, "scores": "bf16 N(0,1/D)"},
+        },
+        "parts_ms": {"design": round(ms_design, 4), "coeffs": round(ms_coeffs, 4),
+                     "wgrad": round(ms_wgrad, 4), "audit": round(ms_audit, 4)},
+        "dense_equiv_GBps": round(bytes_dense / (ms_chain * 1e-3) / 1e9, 1),
+        "roofline": roof_w,
+        "audit": {"value": round(Ba * R / (ms_audit * 1e-3), 1),
+                  "unit": "replicate-estimates/s", "roofline": roof_a},
+    }
+    if not args.no_cpu_baseline:
+        _log("[bench] timing the CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(meta, w, scores, meta_a, wa, scores_a)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

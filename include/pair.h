@@ -1,0 +1,186 @@
+/*
+ * pair.h -- C ABI of libpair: the data-parallel hot path of PAIR
+ * (Pairwise-Aware Inclusion Reweighting) on AMD Instinct MI355X (gfx950).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every array argument is a DEVICE pointer owned by the caller.  The library
+ *    never allocates, frees or retains caller memory; scratch space is passed
+ *    in explicitly (pair_audit's workspace).
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    All work is enqueued asynchronously on it; nothing blocks the host.
+ *  - Host-detectable argument errors return a negative PAIR_E* code and
+ *    enqueue nothing.  A failed launch returns PAIR_EHIP.
+ *  - Data-dependent errors found on the device are OR-ed into *d_status
+ *    (device int32, optional: NULL disables reporting) as PAIR_ST_* bits; the
+ *    outputs of the affected prompt are then unspecified.  Callers that pass
+ *    d_status clear it before the call.
+ *  - Prompts are packed ragged: `offsets` is int64 [B+1] with offsets[0] = 0,
+ *    offsets[B] = nv; prompt b owns packed vertices (rollouts)
+ *    offsets[b] .. offsets[b+1]-1, and G_b = offsets[b+1] - offsets[b].
+ *  - Joint inclusion probabilities are a dense fp32 block per prompt,
+ *    pi[B][gmax][gmax]; entry (i, j) with i < j defines rho_ij = rho_ji (the
+ *    upper triangle is the only part read); the diagonal and the entries
+ *    beyond G_b are ignored on input.
+ *  - Scores are row-major [nv][ld] (ld >= D elements) in fp32 or bf16; the
+ *    base pointer and every row must be 16-byte aligned.
+ *  - Calls are deterministic: the same inputs give bitwise-identical outputs
+ *    (no floating-point atomics).  Concurrent calls on different streams
+ *    share no library state.
+ *
+ * Notation follows the paper: G candidate rollouts per prompt, rewards r_i,
+ * continuation indicators J_i, joint inclusion probabilities rho_ij, pair
+ * kernel h_ij = 1/2 (r_i - r_j)(s_i - s_j), M = C(G, 2).
+ */
+#ifndef PAIR_H
+#define PAIR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define PAIR_OK 0
+#define PAIR_EINVAL (-1)     /* null pointer or malformed size                 */
+#define PAIR_EDTYPE (-2)     /* unknown score dtype                             */
+#define PAIR_ERANGE (-3)     /* gmax outside [2, 64], D < 1, R < 1, ld < D ...  */
+#define PAIR_EALIGN (-4)     /* scores base or row stride not 16-byte aligned   */
+#define PAIR_EHIP (-5)       /* a HIP launch or runtime call failed             */
+#define PAIR_EWORKSPACE (-6) /* workspace missing, misaligned or too small      */
+
+/* Score dtypes. */
+#define PAIR_F32 0
+#define PAIR_BF16 1
+
+/* Device status bits (OR-ed into *d_status). */
+#define PAIR_ST_BAD_GROUP 1  /* G_b < 2, G_b > gmax or offsets not monotone    */
+#define PAIR_ST_RHO_RANGE 2  /* an OBSERVED edge has rho outside (0, 1]        */
+#define PAIR_ST_P_RANGE 4    /* a continuation probability outside (0, 1]      */
+
+/* Largest group size supported by the design draw, the coefficient fold and
+ * the audit (one 64-lane wavefront holds one prompt's vertices). */
+#define PAIR_GMAX_LIMIT 64
+
+/*
+ * pair_design_inclusion -- randomized continuation design (paper Sec. 2.3,
+ * Algorithm 1 "draw J_i with fresh randomization"; Theorem 2's requirement
+ * that rho_ij is logged before rewards are seen).
+ *
+ * Independent Bernoulli vertices: J_i ~ Bernoulli(p_i), I_ij = J_i J_j,
+ * rho_ij = p_i p_j.  The indicators come from the counter-based generator
+ * Philox4x64-10 (Salmon et al., SC'11):
+ *     key = (seed, 0), counter = (rep0 + r, b, i >> 2, 0),
+ *     u   = top 32 bits of output word (i & 3),
+ *     J_i = [u < floor(p_i * 2^32)]    (p_i = 1 always includes),
+ * so P(J_i = 1) = p_i exactly for every fp32 p_i >= 2^-9, and any range of
+ * replicates can be regenerated independently (resumable, shardable).
+ *
+ *   B, nv, gmax   prompts, packed vertices, dense block size (2 <= gmax <= 64)
+ *   offsets       int64 [B+1]
+ *   p             fp32 [nv] continuation probabilities in (0, 1]
+ *   seed, rep0, R generator key, first replicate index, replicate count (R >= 1)
+ *   mask          uint8 [R][nv] out: J for replicate rep0 + r       (or NULL)
+ *   pi            fp32 [B][gmax][gmax] out: logged rho_ij = fl32(p_i p_j) for
+ *                 i != j, p_i on the diagonal, 0 beyond G_b        (or NULL)
+ *   edge_count    int32 [R][B] out: observed edges K_E = C(k, 2)    (or NULL)
+ *   completed     int32 [R][B] out: completed vertices k            (or NULL)
+ * Device status: PAIR_ST_BAD_GROUP, PAIR_ST_P_RANGE.
+ */
+int pair_design_inclusion(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                          const float* p, uint64_t seed, int64_t rep0, int64_t R,
+                          uint8_t* mask, float* pi, int32_t* edge_count, int32_t* completed,
+                          int32_t* d_status, void* stream);
+
+/*
+ * pair_edge_coeffs -- pair-corrected sequence advantages, paper Eq.
+ * (pair-advantage) with the enumeration of Algorithm 1 ("accumulate
+ * h_ij / rho_ij into A~_i, A~_j") and App. C's numerics (fp32 accumulation,
+ * centred across the observed endpoints):
+ *     A~_i = J_i / (2M) * sum_{j != i} J_j (r_i - r_j) / rho_ij,
+ * then A~_i -= mean of A~ over completed vertices.  Unobserved vertices get
+ * exactly 0, and so does every vertex of a prompt with fewer than two
+ * completed vertices (App. B) or with equal observed rewards.  M = C(G_b, 2)
+ * counts the candidate pool, not the observed edges.
+ *
+ *   rewards       fp32 [nv]
+ *   mask          uint8 [nv] completion indicators J (NULL: all completed)
+ *   pi            fp32 [B][gmax][gmax] logged rho (NULL: rho = 1, i.e. the
+ *                 unweighted estimator / the complete-pair coefficients)
+ *   coeff         fp32 [nv] out: A~
+ *   edge_count    int32 [B] out: observed edges K_E                 (or NULL)
+ * Device status: PAIR_ST_BAD_GROUP, PAIR_ST_RHO_RANGE.
+ */
+int pair_edge_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                     const float* rewards, const uint8_t* mask, const float* pi, float* coeff,
+                     int32_t* edge_count, int32_t* d_status, void* stream);
+
+/*
+ * pair_weighted_grad -- the induced-edge HT gradient, paper Eq. (pair-ht)
+ * written as sum_i A~_i s_i (Sec. 3.5), batched over prompts:
+ *     out[b][d] = sum_{i < G_b} coeff[offsets[b] + i] * s[offsets[b] + i][d]
+ * with fp32 accumulation in a fixed order.  Rows whose coefficient is exactly
+ * zero (unobserved rollouts, saturated prompts) are neither read nor summed:
+ * an uncompleted rollout has no score, so its row may hold anything.
+ *
+ *   D, scores, dtype, ld   score block (PAIR_F32 or PAIR_BF16), row stride ld
+ *   coeff          fp32 [nv] (from pair_edge_coeffs)
+ *   out            fp32 [B][D] out (rows packed with stride D)
+ * Any G_b >= 0 is accepted here.  Device status: PAIR_ST_BAD_GROUP
+ * (offsets not monotone or beyond nv: that prompt's row is not written).
+ */
+int pair_weighted_grad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D,
+                       const void* scores, int32_t dtype, int64_t ld, const float* coeff,
+                       float* out, int32_t* d_status, void* stream);
+
+/*
+ * pair_audit_workspace_bytes -- device workspace that pair_audit needs for
+ * B prompts of at most gmax vertices, D score columns and R replicates.
+ */
+size_t pair_audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R);
+
+/*
+ * pair_audit -- frozen-population estimator audit (paper Sec. 5.2, Table 2,
+ * App. D metrics).  For each prompt the complete candidate population is
+ * fixed; R design replicates rep0 .. rep0+R-1 are drawn exactly as
+ * pair_design_inclusion draws them (same seed => same masks), each one gives
+ * the HT estimate g_r = sum_i A~^(r)_i s_i, and against the complete-pair
+ * target t = sum_i a_i s_i, a_i = A~ with every vertex completed and rho = 1
+ * (= (r_i - mean r)/(G - 1), Theorem 1):
+ *     e_r  = || g_r - t ||^2 = || (A~^(r) - a) S_b ||^2
+ *     mse  = (1/R) sum_r e_r
+ *     bias = || (1/R) sum_r g_r - t ||
+ * The R x D estimates are never materialised: (A~^(r) - a), rounded to bf16,
+ * times S_b runs on bf16 matrix cores with the squared norm reduced in the
+ * epilogue.  Weights use rho = pi_w when given (e.g. all ones replays the
+ * unweighted estimator of Prop. 1), else the logged fl32(p_i p_j).
+ *
+ *   scores, dtype  PAIR_BF16 only (the matrix-core operand type)
+ *   rewards, p     fp32 [nv]
+ *   pi_w           fp32 [B][gmax][gmax] rho used in the weights      (or NULL)
+ *   mse, bias_norm fp64 [B] out
+ *   rep_sqerr      fp32 [B][R] out: e_r                              (or NULL)
+ *   edge_count     int32 [B][R] out: observed edges per replicate    (or NULL)
+ *   workspace      device scratch of ws_bytes >= pair_audit_workspace_bytes,
+ *                  256-byte aligned; contents on entry do not matter
+ * Device status: PAIR_ST_BAD_GROUP, PAIR_ST_P_RANGE, PAIR_ST_RHO_RANGE.
+ */
+int pair_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+               const void* scores, int32_t dtype, int64_t ld, const float* rewards,
+               const float* p, const float* pi_w, uint64_t seed, int64_t rep0, int64_t R,
+               double* mse, double* bias_norm, float* rep_sqerr, int32_t* edge_count,
+               void* workspace, size_t ws_bytes, int32_t* d_status, void* stream);
+
+/* Human-readable text for a return code. */
+const char* pair_strerror(int code);
+
+/* Library ABI version (major * 10000 + minor * 100 + patch). */
+int pair_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PAIR_H */

@@ -1,0 +1,237 @@
+"""PAIR hot path on AMD Instinct MI355X: thin Python binding over libpair.so.
+
+Each ``pair_*`` function mirrors the C entry point of the same name declared
+in ``include/pair.h``: it checks device, dtype and contiguity of the torch
+tensors it is given, passes their device pointers and the current HIP stream,
+and turns a negative return code into :class:`PairError`.  Every step of the
+computation runs in the library's HIP kernels; torch only provides device
+memory and the stream.  There is no fallback: if ``libpair.so`` is missing the
+import of the library fails loudly (build it with
+``python -m paper_2608_11368_amd.build``).
+
+The lower-case helpers (``design_inclusion``, ``edge_coeffs``,
+``weighted_grad``, ``audit``) allocate the outputs with torch and call the
+``pair_*`` functions.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpair.so")
+
+PAIR_F32 = 0
+PAIR_BF16 = 1
+ST_BAD_GROUP = 1
+ST_RHO_RANGE = 2
+ST_P_RANGE = 4
+GMAX_LIMIT = 64
+
+EXPORTED = ("pair_design_inclusion", "pair_edge_coeffs", "pair_weighted_grad",
+            "pair_audit_workspace_bytes", "pair_audit", "pair_strerror", "pair_version")
+
+
+class PairError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {strerror(code)} (code {code})")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libpair.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2608_11368_amd.build` (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.c_void_p
+        i64, i32, u64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
+        L.pair_design_inclusion.argtypes = [i64, i64, i32, P, P, u64, i64, i64, P, P, P, P, P, P]
+        L.pair_design_inclusion.restype = ctypes.c_int
+        L.pair_edge_coeffs.argtypes = [i64, i64, i32, P, P, P, P, P, P, P, P]
+        L.pair_edge_coeffs.restype = ctypes.c_int
+        L.pair_weighted_grad.argtypes = [i64, i64, P, i64, P, i32, i64, P, P, P, P]
+        L.pair_weighted_grad.restype = ctypes.c_int
+        L.pair_audit_workspace_bytes.argtypes = [i64, i32, i64, i64]
+        L.pair_audit_workspace_bytes.restype = ctypes.c_size_t
+        L.pair_audit.argtypes = [i64, i64, i32, P, i64, P, i32, i64, P, P, P, u64, i64, i64,
+                                 P, P, P, P, P, ctypes.c_size_t, P, P]
+        L.pair_audit.restype = ctypes.c_int
+        L.pair_strerror.argtypes = [ctypes.c_int]
+        L.pair_strerror.restype = ctypes.c_char_p
+        L.pair_version.argtypes = []
+        L.pair_version.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def strerror(code: int) -> str:
+    return lib().pair_strerror(int(code)).decode()
+
+
+def version() -> int:
+    return lib().pair_version()
+
+
+# ----------------------------------------------------------- marshalling ---
+def _dev(t, name, dtype, numel=None, allow_none=False):
+    if t is None:
+        if allow_none:
+            return None
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, needs {numel}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _scores_arg(scores):
+    if not isinstance(scores, torch.Tensor) or scores.device.type != "cuda" or scores.dim() != 2:
+        raise ValueError("scores must be a 2-D CUDA tensor [nv][ld-strided rows]")
+    if scores.stride(1) != 1:
+        raise ValueError("scores rows must be contiguous")
+    if scores.dtype == torch.float32:
+        code = PAIR_F32
+    elif scores.dtype == torch.bfloat16:
+        code = PAIR_BF16
+    else:
+        raise TypeError("scores must be float32 or bfloat16")
+    return ctypes.c_void_p(scores.data_ptr()), code, scores.stride(0), scores.shape[1]
+
+
+def _rc(code, where):
+    if code != 0:
+        raise PairError(code, where)
+
+
+# ------------------------------------------------------- C-ABI mirrors -----
+def pair_design_inclusion(B, nv, gmax, offsets, p, seed, rep0, R, mask=None, pi=None,
+                          edge_count=None, completed=None, d_status=None, stream=None):
+    _rc(lib().pair_design_inclusion(
+        B, nv, gmax, _dev(offsets, "offsets", torch.int64, B + 1), _dev(p, "p", torch.float32, nv),
+        ctypes.c_uint64(seed & ((1 << 64) - 1)), rep0, R,
+        _dev(mask, "mask", torch.uint8, R * nv, True),
+        _dev(pi, "pi", torch.float32, B * gmax * gmax, True),
+        _dev(edge_count, "edge_count", torch.int32, R * B, True),
+        _dev(completed, "completed", torch.int32, R * B, True),
+        _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_design_inclusion")
+
+
+def pair_edge_coeffs(B, nv, gmax, offsets, rewards, mask, pi, coeff, edge_count=None,
+                     d_status=None, stream=None):
+    _rc(lib().pair_edge_coeffs(
+        B, nv, gmax, _dev(offsets, "offsets", torch.int64, B + 1),
+        _dev(rewards, "rewards", torch.float32, nv), _dev(mask, "mask", torch.uint8, nv, True),
+        _dev(pi, "pi", torch.float32, B * gmax * gmax, True),
+        _dev(coeff, "coeff", torch.float32, nv),
+        _dev(edge_count, "edge_count", torch.int32, B, True),
+        _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_edge_coeffs")
+
+
+def pair_weighted_grad(B, nv, offsets, scores, coeff, out, d_status=None, stream=None):
+    sp, code, ld, D = _scores_arg(scores)
+    _rc(lib().pair_weighted_grad(
+        B, nv, _dev(offsets, "offsets", torch.int64, B + 1), D, sp, code, ld,
+        _dev(coeff, "coeff", torch.float32, nv), _dev(out, "out", torch.float32, B * D),
+        _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_weighted_grad")
+
+
+def pair_audit_workspace_bytes(B, gmax, D, R) -> int:
+    return int(lib().pair_audit_workspace_bytes(B, gmax, D, R))
+
+
+def pair_audit(B, nv, gmax, offsets, scores, rewards, p, pi_w, seed, rep0, R, mse, bias_norm,
+               rep_sqerr, edge_count, workspace, d_status=None, stream=None):
+    sp, code, ld, D = _scores_arg(scores)
+    ws = _dev(workspace, "workspace", torch.uint8)
+    _rc(lib().pair_audit(
+        B, nv, gmax, _dev(offsets, "offsets", torch.int64, B + 1), D, sp, code, ld,
+        _dev(rewards, "rewards", torch.float32, nv), _dev(p, "p", torch.float32, nv),
+        _dev(pi_w, "pi_w", torch.float32, B * gmax * gmax, True),
+        ctypes.c_uint64(seed & ((1 << 64) - 1)), rep0, R,
+        _dev(mse, "mse", torch.float64, B), _dev(bias_norm, "bias_norm", torch.float64, B),
+        _dev(rep_sqerr, "rep_sqerr", torch.float32, B * R, True),
+        _dev(edge_count, "edge_count", torch.int32, B * R, True),
+        ws, workspace.numel(), _dev(d_status, "d_status", torch.int32, 1, True),
+        _stream(stream)), "pair_audit")
+
+
+# ------------------------------------------------ allocating helpers -------
+def _nv(offsets):
+    return int(offsets[-1].item())
+
+
+def design_inclusion(offsets, p, seed, rep0, R, gmax, want_mask=True, want_pi=True, nv=None,
+                     stream=None):
+    B = offsets.numel() - 1
+    nv = _nv(offsets) if nv is None else nv
+    dev = p.device
+    out = {
+        "mask": torch.empty((R, nv), dtype=torch.uint8, device=dev) if want_mask else None,
+        "pi": torch.empty((B, gmax, gmax), dtype=torch.float32, device=dev) if want_pi else None,
+        "edge_count": torch.empty((R, B), dtype=torch.int32, device=dev),
+        "completed": torch.empty((R, B), dtype=torch.int32, device=dev),
+        "status": torch.zeros(1, dtype=torch.int32, device=dev),
+    }
+    pair_design_inclusion(B, nv, gmax, offsets, p, seed, rep0, R, out["mask"], out["pi"],
+                          out["edge_count"], out["completed"], out["status"], stream)
+    return out
+
+
+def edge_coeffs(offsets, rewards, mask, pi, gmax, nv=None, stream=None):
+    B = offsets.numel() - 1
+    nv = _nv(offsets) if nv is None else nv
+    dev = rewards.device
+    coeff = torch.empty(nv, dtype=torch.float32, device=dev)
+    ec = torch.empty(B, dtype=torch.int32, device=dev)
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+    pair_edge_coeffs(B, nv, gmax, offsets, rewards, mask, pi, coeff, ec, st, stream)
+    return {"coeff": coeff, "edge_count": ec, "status": st}
+
+
+def weighted_grad(offsets, scores, coeff, nv=None, stream=None):
+    B = offsets.numel() - 1
+    nv = _nv(offsets) if nv is None else nv
+    D = scores.shape[1]
+    out = torch.empty((B, D), dtype=torch.float32, device=scores.device)
+    st = torch.zeros(1, dtype=torch.int32, device=scores.device)
+    pair_weighted_grad(B, nv, offsets, scores, coeff, out, st, stream)
+    return {"out": out, "status": st}
+
+
+def audit(offsets, scores, rewards, p, seed, rep0, R, gmax, pi_w=None, want_reps=True, nv=None,
+          workspace=None, stream=None):
+    B = offsets.numel() - 1
+    nv = _nv(offsets) if nv is None else nv
+    dev = scores.device
+    need = pair_audit_workspace_bytes(B, gmax, scores.shape[1], R)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    out = {
+        "mse": torch.empty(B, dtype=torch.float64, device=dev),
+        "bias_norm": torch.empty(B, dtype=torch.float64, device=dev),
+        "rep_sqerr": torch.empty((B, R), dtype=torch.float32, device=dev) if want_reps else None,
+        "edge_count": torch.empty((B, R), dtype=torch.int32, device=dev) if want_reps else None,
+        "status": torch.zeros(1, dtype=torch.int32, device=dev),
+    }
+    pair_audit(B, nv, gmax, offsets, scores, rewards, p, pi_w, seed, rep0, R, out["mse"],
+               out["bias_norm"], out["rep_sqerr"], out["edge_count"], workspace, out["status"],
+               stream)
+    return out

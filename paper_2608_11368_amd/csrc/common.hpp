@@ -1,0 +1,116 @@
+// Device helpers shared by the libpair kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/pair.h"
+
+namespace pair {
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// Philox4x64-10 counter-based generator (Salmon, Moraes, Dror, Shaw, SC'11).
+// Ten rounds; each round forms the full 128-bit products of counter words 0
+// and 2 with the two round multipliers, then the new state is
+//   (hi(m1*x2) ^ x1 ^ k0, lo(m1*x2), hi(m0*x0) ^ x3 ^ k1, lo(m0*x0)),
+// and the key advances by the two Weyl increments between rounds.
+// ---------------------------------------------------------------------------
+struct Philox4x64 {
+  uint64_t w[4];
+};
+
+__device__ __forceinline__ Philox4x64 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2,
+                                                    uint64_t c3, uint64_t k0, uint64_t k1) {
+  const uint64_t m0 = 0xD2E7470EE14C6C93ull, m1 = 0xCA5A826395121157ull;
+  const uint64_t w0 = 0x9E3779B97F4A7C15ull, w1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) {
+      k0 += w0;
+      k1 += w1;
+    }
+    const uint64_t hi0 = __umul64hi(m0, c0), lo0 = m0 * c0;
+    const uint64_t hi1 = __umul64hi(m1, c2), lo1 = m1 * c2;
+    const uint64_t n0 = hi1 ^ c1 ^ k0;
+    const uint64_t n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+  }
+  Philox4x64 o;
+  o.w[0] = c0;
+  o.w[1] = c1;
+  o.w[2] = c2;
+  o.w[3] = c3;
+  return o;
+}
+
+// Inclusion threshold floor(p * 2^32) as a 33-bit integer; p >= 1 includes always.
+__device__ __forceinline__ uint64_t inclusion_threshold(float p) {
+  if (p >= 1.0f) return 0x100000000ull;
+  return (uint64_t)(p * 4294967296.0f);  // exact scaling by 2^32, truncation = floor
+}
+
+__device__ __forceinline__ bool p_in_range(float p) { return p > 0.0f && p <= 1.0f; }
+
+// Non-temporal 16-byte global accesses for data streamed exactly once.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 load_nt16(const void* src) {
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(src));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ void store_nt16(void* dst, float a, float b, float c, float d) {
+  f32x4_t v = {a, b, c, d};
+  __builtin_nontemporal_store(v, reinterpret_cast<f32x4_t*>(dst));
+}
+
+// bf16 <-> fp32 bit conversions.
+__device__ __forceinline__ float bf16lo_to_f32(uint32_t pair) { return __uint_as_float(pair << 16); }
+__device__ __forceinline__ float bf16hi_to_f32(uint32_t pair) {
+  return __uint_as_float(pair & 0xffff0000u);
+}
+// Round-to-nearest-even fp32 -> bf16 (finite inputs; NaN kept quiet).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Butterfly sum across the 64 lanes: every lane ends with the same bits
+// (IEEE addition is commutative, so partner lanes form identical sums).
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) v += __shfl_xor(v, m, kWave);
+  return v;
+}
+
+__device__ __forceinline__ void raise_status(int32_t* d_status, int32_t bits) {
+  if (d_status != nullptr) atomicOr(d_status, bits);
+}
+
+// Validated bounds of prompt b: returns false (and sets the status bit) when
+// the offsets are not monotone, leave [0, nv], or G_b is outside [gmin, gmax].
+__device__ __forceinline__ bool prompt_bounds(const int64_t* offsets, int64_t b, int64_t nv,
+                                              int64_t gmin, int64_t gmax, int64_t* o0,
+                                              int64_t* g, int32_t* d_status, bool report) {
+  const int64_t a = offsets[b], e = offsets[b + 1];
+  const bool ok = a >= 0 && e >= a && e <= nv && (e - a) >= gmin && (e - a) <= gmax;
+  if (!ok) {
+    if (report) raise_status(d_status, PAIR_ST_BAD_GROUP);
+    *o0 = 0;
+    *g = 0;
+    return false;
+  }
+  *o0 = a;
+  *g = e - a;
+  return true;
+}
+
+}  // namespace pair

@@ -1,0 +1,92 @@
+// Design draw: independent Bernoulli continuation indicators and the logged
+// joint inclusion probabilities (paper Sec. 2.3; Algorithm 1, "draw J_i with
+// fresh randomization"; rho_ij must be logged before rewards, Theorem 2).
+//
+// One 64-lane wavefront per (replicate, prompt) unit, lane i = vertex i.  Each
+// lane evaluates Philox4x64-10 at counter (r, b, i >> 2, 0) and keeps word
+// i & 3 (lanes of one group of four compute the same block in lockstep, so
+// this costs one generator evaluation per unit).  Completed-vertex and edge
+// counts come from a ballot + popcount.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace pair {
+
+__global__ __launch_bounds__(256) void design_draw_kernel(
+    int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets,
+    const float* __restrict__ p, uint64_t seed, int64_t rep0, int64_t R, uint8_t* __restrict__ mask,
+    int32_t* __restrict__ edge_count, int32_t* __restrict__ completed, int32_t* d_status) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t units = B * R;
+  const int64_t waves_total = (int64_t)gridDim.x * (blockDim.x / kWave);
+  for (int64_t u = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave; u < units;
+       u += waves_total) {
+    const int64_t r = u / B;  // replicate-major: consecutive waves share r
+    const int64_t b = u - r * B;
+    int64_t o0, g;
+    if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, d_status, r == 0)) continue;
+    const bool active = lane < g;
+    int J = 0;
+    if (active) {
+      const float pv = p[o0 + lane];
+      const Philox4x64 x = philox4x64_10((uint64_t)(rep0 + r), (uint64_t)b, (uint64_t)(lane >> 2),
+                                         0ull, seed, 0ull);
+      const uint64_t u32 = x.w[lane & 3] >> 32;
+      if (p_in_range(pv)) {
+        J = u32 < inclusion_threshold(pv) ? 1 : 0;
+      } else if (r == 0) {
+        raise_status(d_status, PAIR_ST_P_RANGE);
+      }
+      if (mask != nullptr) mask[r * nv + o0 + lane] = (uint8_t)J;
+    }
+    const uint64_t bits = __ballot(J != 0);
+    if (lane == 0) {
+      const int32_t k = (int32_t)__popcll(bits);
+      if (completed != nullptr) completed[r * B + b] = k;
+      if (edge_count != nullptr) edge_count[r * B + b] = k * (k - 1) / 2;
+    }
+  }
+}
+
+// Logged rho block per prompt: rho_ij = fl32(p_i * p_j) off the diagonal,
+// p_i on it, zero outside the G_b x G_b corner.
+__global__ __launch_bounds__(256) void design_pi_kernel(int64_t B, int64_t nv, int32_t gmax,
+                                                        const int64_t* __restrict__ offsets,
+                                                        const float* __restrict__ p,
+                                                        float* __restrict__ pi) {
+  const int64_t b = blockIdx.x;
+  if (b >= B) return;
+  const int64_t a = offsets[b], e = offsets[b + 1];
+  const bool ok = a >= 0 && e >= a && e <= nv && (e - a) >= 2 && (e - a) <= gmax;
+  const int64_t g = ok ? e - a : 0;
+  const int64_t n = (int64_t)gmax * gmax;
+  float* blk = pi + b * n;
+  for (int64_t idx = threadIdx.x; idx < n; idx += blockDim.x) {
+    const int64_t i = idx / gmax, j = idx - i * gmax;
+    float v = 0.0f;
+    if (i < g && j < g) v = (i == j) ? p[a + i] : p[a + i] * p[a + j];
+    blk[idx] = v;
+  }
+}
+
+int launch_design(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, const float* p,
+                  uint64_t seed, int64_t rep0, int64_t R, uint8_t* mask, float* pi,
+                  int32_t* edge_count, int32_t* completed, int32_t* d_status, hipStream_t stream) {
+  if (pi != nullptr) {
+    hipLaunchKernelGGL(design_pi_kernel, dim3((unsigned)B), dim3(256), 0, stream, B, nv, gmax,
+                       offsets, p, pi);
+    if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
+  }
+  if (mask != nullptr || edge_count != nullptr || completed != nullptr) {
+    const int64_t units = B * R;
+    const int64_t blocks_needed = (units + 3) / 4;
+    const int64_t cap = (int64_t)device_cu_count() * 32;
+    const unsigned grid = (unsigned)(blocks_needed < cap ? blocks_needed : cap);
+    hipLaunchKernelGGL(design_draw_kernel, dim3(grid), dim3(256), 0, stream, B, nv, gmax, offsets,
+                       p, seed, rep0, R, mask, edge_count, completed, d_status);
+    if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
+  }
+  return PAIR_OK;
+}
+
+}  // namespace pair

@@ -1,0 +1,34 @@
+// Internal host-side launchers (C++ linkage, not exported).  Arguments are
+// validated by the C entry points in api.hip before any of these run.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pair {
+
+// Compute units of the current device (cached per device).
+int device_cu_count();
+
+int launch_design(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, const float* p,
+                  uint64_t seed, int64_t rep0, int64_t R, uint8_t* mask, float* pi,
+                  int32_t* edge_count, int32_t* completed, int32_t* d_status, hipStream_t stream);
+
+int launch_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                  const float* rewards, const uint8_t* mask, const float* pi, float* coeff,
+                  int32_t* edge_count, int32_t* d_status, hipStream_t stream);
+
+int launch_wgrad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D, const void* scores,
+                 int32_t dtype, int64_t ld, const float* coeff, float* out, int32_t* d_status,
+                 hipStream_t stream);
+
+size_t audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R);
+
+int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                 const void* scores, int64_t ld, const float* rewards, const float* p,
+                 const float* pi_w, uint64_t seed, int64_t rep0, int64_t R, double* mse,
+                 double* bias_norm, float* rep_sqerr, int32_t* edge_count, void* workspace,
+                 int32_t* d_status, hipStream_t stream);
+
+}  // namespace pair

@@ -1,0 +1,126 @@
+"""C-ABI checks that need no GPU: libpair.so loads, exports every entry point
+declared in include/pair.h, and rejects malformed arguments on the host
+before anything is enqueued (these calls never reach the HIP runtime)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2608_11368_amd as pair
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pair.h")
+
+FAKE = ctypes.c_void_p(1 << 20)           # 16-byte aligned non-null stand-in, never dereferenced
+ODD = ctypes.c_void_p((1 << 20) + 2)      # misaligned stand-in
+NULL = None
+
+
+def _declared():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:int|size_t|const char\*)\s+(pair_\w+)\(", src, re.M)))
+
+
+def test_header_declares_the_four_calls():
+    names = _declared()
+    for n in ("pair_design_inclusion", "pair_edge_coeffs", "pair_weighted_grad", "pair_audit"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = pair.lib()
+    names = _declared()
+    assert names
+    for n in names:
+        assert hasattr(L, n), n
+    dyn = subprocess.run(["nm", "-D", "--defined-only", pair.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s+(pair_\w+)$", dyn, re.M))
+    assert set(names) <= exported
+    assert set(pair.EXPORTED) == set(names)
+
+
+def test_version_and_strerror():
+    assert pair.version() >= 100
+    for code in (0, -1, -2, -3, -4, -5, -6, -99):
+        assert isinstance(pair.strerror(code), str) and pair.strerror(code)
+
+
+def test_design_inclusion_rejects_bad_arguments():
+    L = pair.lib()
+    f = L.pair_design_inclusion
+    ok = dict(B=4, nv=32, gmax=8, offsets=FAKE, p=FAKE, seed=1, rep0=0, R=1, mask=FAKE, pi=NULL,
+              ec=NULL, comp=NULL, st=NULL, stream=NULL)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["B"], a["nv"], a["gmax"], a["offsets"], a["p"], a["seed"], a["rep0"], a["R"],
+                 a["mask"], a["pi"], a["ec"], a["comp"], a["st"], a["stream"])
+
+    assert call(offsets=NULL) == -1
+    assert call(p=NULL) == -1
+    assert call(B=0) == -1
+    assert call(gmax=1) == -3
+    assert call(gmax=65) == -3
+    assert call(R=0) == -3
+    assert call(rep0=-1) == -3
+    assert call(mask=NULL) == -1          # nothing to produce
+
+
+def test_edge_coeffs_rejects_bad_arguments():
+    f = pair.lib().pair_edge_coeffs
+    assert f(4, 32, 8, NULL, FAKE, NULL, NULL, FAKE, NULL, NULL, NULL) == -1
+    assert f(4, 32, 8, FAKE, NULL, NULL, NULL, FAKE, NULL, NULL, NULL) == -1
+    assert f(4, 32, 8, FAKE, FAKE, NULL, NULL, NULL, NULL, NULL, NULL) == -1
+    assert f(4, 32, 100, FAKE, FAKE, NULL, NULL, FAKE, NULL, NULL, NULL) == -3
+    assert f(-1, 32, 8, FAKE, FAKE, NULL, NULL, FAKE, NULL, NULL, NULL) == -1
+
+
+def test_weighted_grad_rejects_bad_arguments():
+    f = pair.lib().pair_weighted_grad
+
+    def call(B=4, nv=32, off=FAKE, D=64, s=FAKE, dt=1, ld=64, c=FAKE, out=FAKE):
+        return f(B, nv, off, D, s, dt, ld, c, out, NULL, NULL)
+
+    assert call(off=NULL) == -1
+    assert call(s=NULL) == -1
+    assert call(c=NULL) == -1
+    assert call(out=NULL) == -1
+    assert call(dt=7) == -2
+    assert call(D=0) == -3
+    assert call(ld=63) == -3
+    assert call(s=ODD) == -4
+    assert call(ld=66) == -4              # bf16 rows of 132 bytes are not 16-byte aligned
+    assert call(dt=0, ld=66) == -4        # fp32 rows of 264 bytes are not 16-byte aligned
+
+
+def test_audit_rejects_bad_arguments_and_sizes_workspace():
+    L = pair.lib()
+    need = L.pair_audit_workspace_bytes(256, 16, 65536, 4096)
+    assert need > 256 * 4096 * 16 * 2                     # bf16 deviations at least
+    assert L.pair_audit_workspace_bytes(4, 65, 64, 10) == 0
+    assert L.pair_audit_workspace_bytes(4, 8, 64, 0) == 0
+    f = L.pair_audit
+
+    def call(dt=1, ws=FAKE, wsb=need, R=4096, gmax=16, mse=FAKE, s=FAKE):
+        return f(256, 4096, gmax, FAKE, 65536, s, dt, 65536, FAKE, FAKE, NULL, 1, 0, R, mse, FAKE,
+                 NULL, NULL, ws, wsb, NULL, NULL)
+
+    assert call(dt=0) == -2               # the matrix-core path takes bf16 scores
+    assert call(ws=NULL) == -6
+    assert call(wsb=need - 1) == -6
+    assert call(ws=ctypes.c_void_p((1 << 20) + 16)) == -6   # workspace must be 256-byte aligned
+    assert call(R=0) == -3
+    assert call(gmax=80) == -3
+    assert call(mse=NULL) == -1
+    assert call(s=ODD) == -4
+
+
+def test_binding_checks_tensors_before_calling():
+    import torch
+
+    t = torch.zeros(4)
+    with pytest.raises(ValueError):
+        pair._dev(t, "x", torch.float32)          # host tensor is refused

@@ -1,0 +1,430 @@
+"""GPU parity: the HIP path, called through the C ABI, against the CPU oracle.
+
+Bars (stated by the task for this estimator):
+  - masks, completed counts, edge counts, logged rho: bit-exact
+  - gradients / coefficients: relative L2 <= 1e-5 for fp32 scores,
+    <= 2e-3 for bf16 scores (fp32 accumulation on the GPU, fp64 in the oracle)
+  - prompts whose estimate is exactly zero (saturated rewards, < 2 completed
+    vertices) are exactly zero on the GPU
+  - audit: per-replicate squared errors, MSE and bias norm within 2e-3
+    relative (bf16 matrix-core operands), edge counts bit-exact
+Full-size workloads are checked on sampled columns / prompts, plus
+properties that hold at any size.
+"""
+import math
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_11368_amd as pair
+import workloads as wl
+from tests.gpu_util import DEV, log, rel_l2, scores_to_device, scores_to_host, upload_meta
+
+pytestmark = pytest.mark.gpu
+
+FP32_TOL = 1e-5
+BF16_TOL = 2e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    pair.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _chain_gpu(meta, dm, scores, seed, gmax, rep=0):
+    """design draw -> coefficients -> weighted gradient, all through the C ABI."""
+    B, nv = meta.B, meta.nv
+    d = pair.design_inclusion(dm["offsets"], dm["p"], seed, rep, 1, gmax, nv=nv)
+    c = pair.edge_coeffs(dm["offsets"], dm["rewards"], d["mask"][0], d["pi"], gmax, nv=nv)
+    g = pair.weighted_grad(dm["offsets"], scores, c["coeff"], nv=nv)
+    torch.cuda.synchronize()
+    return d, c, g
+
+
+def _chain_oracle(meta, scores_host, seed, gmax, rep=0):
+    d = oracle.design_inclusion(meta.offsets, meta.p, seed, rep, 1, gmax)
+    est, ec = oracle.pair_grad(meta.offsets, scores_host, meta.rewards, d["mask"][0], d["pi"])
+    return d, est, ec
+
+
+def _assert_zero_rows(meta, coeff_gpu, out_gpu):
+    c = coeff_gpu.cpu().numpy()
+    for b in range(meta.B):
+        o0, o1 = meta.offsets[b], meta.offsets[b + 1]
+        if not np.any(c[o0:o1]):
+            assert float(out_gpu[b].abs().max()) == 0.0, f"prompt {b} must be exactly zero"
+
+
+# ------------------------------------------------------------ design draw --
+@pytest.mark.parametrize("name,B,R,rep0", [("tiny", None, 1, 0), ("ragged", None, 3, 5),
+                                           ("audit", 64, 40, 1000), ("b128", None, 2, 0)])
+def test_design_draw_bit_exact(name, B, R, rep0):
+    w = wl.WORKLOADS[name]
+    if B:
+        w = w.replace(B=B)
+    meta = wl.host_meta(w)
+    log(f"design draw {name} B={meta.B} R={R} rep0={rep0}")
+    dm = upload_meta(meta)
+    got = pair.design_inclusion(dm["offsets"], dm["p"], w.design_seed, rep0, R, meta.gmax, nv=meta.nv)
+    want = oracle.design_inclusion(meta.offsets, meta.p, w.design_seed, rep0, R, meta.gmax)
+    assert np.array_equal(got["mask"].cpu().numpy(), want["mask"])
+    assert np.array_equal(got["pi"].cpu().numpy(), want["pi"])
+    assert np.array_equal(got["edge_count"].cpu().numpy(), want["edge_count"])
+    assert np.array_equal(got["completed"].cpu().numpy(), want["completed"])
+    assert int(got["status"].item()) == 0
+
+
+# ------------------------------------------------------ coefficient fold --
+@pytest.mark.parametrize("name", ["tiny", "b128", "ragged"])
+def test_edge_coeffs_vs_oracle(name):
+    w = wl.WORKLOADS[name]
+    meta = wl.host_meta(w)
+    log(f"edge coeffs {name} B={meta.B}")
+    dm = upload_meta(meta)
+    d = oracle.design_inclusion(meta.offsets, meta.p, w.design_seed, 0, 1, meta.gmax)
+    mask = torch.from_numpy(d["mask"][0]).to(DEV)
+    pi = torch.from_numpy(d["pi"]).to(DEV)
+    got = pair.edge_coeffs(dm["offsets"], dm["rewards"], mask, pi, meta.gmax, nv=meta.nv)
+    want, ec = oracle.pair_coeffs(meta.offsets, meta.rewards, d["mask"][0], d["pi"])
+    c = got["coeff"].cpu().numpy()
+    err = rel_l2(c, want)
+    log(f"  coeff rel L2 = {err:.3e}")
+    assert err <= FP32_TOL
+    assert np.all(c[want == 0.0] == 0.0)
+    assert np.array_equal(got["edge_count"].cpu().numpy(), ec)
+    # unweighted / complete-pair: rho := 1, every vertex completed
+    full = pair.edge_coeffs(dm["offsets"], dm["rewards"], None, None, meta.gmax, nv=meta.nv)
+    want_full, _ = oracle.pair_coeffs(meta.offsets, meta.rewards)
+    assert rel_l2(full["coeff"].cpu().numpy(), want_full) <= FP32_TOL
+
+
+# --------------------------------------------------- weighted gradient ----
+def test_weighted_grad_tiny_fp32_chain():
+    w = wl.WORKLOADS["tiny"]
+    meta = wl.host_meta(w)
+    log("chain tiny fp32")
+    dm = upload_meta(meta)
+    s = wl.host_scores(w, meta.nv)
+    d, c, g = _chain_gpu(meta, dm, scores_to_device(s, w), w.design_seed, meta.gmax)
+    od, est, ec = _chain_oracle(meta, s, w.design_seed, meta.gmax)
+    assert np.array_equal(d["mask"].cpu().numpy(), od["mask"])
+    assert np.array_equal(c["edge_count"].cpu().numpy(), ec)
+    err = rel_l2(g["out"].cpu().numpy(), est)
+    log(f"  grad rel L2 = {err:.3e}")
+    assert err <= FP32_TOL
+    _assert_zero_rows(meta, c["coeff"], g["out"])
+
+
+@pytest.mark.parametrize("name,B,D,pad", [("b128", 32, 4096 + 37, 24), ("qwen3", 16, 8192 + 5, 0),
+                                          ("ragged", 96, 2048 + 13, 8), ("audit", 24, 1000, 8)])
+def test_weighted_grad_bf16_chain_reduced(name, B, D, pad):
+    w = wl.WORKLOADS[name].replace(B=B, D=D)
+    meta = wl.host_meta(w)
+    ld = (D + 7) // 8 * 8 + pad                     # 16-byte aligned bf16 rows
+    log(f"chain {name} B={B} D={D} ld={ld}")
+    dm = upload_meta(meta)
+    s = wl.host_scores(w, meta.nv, ld=ld)           # NaN in the row padding
+    sd = scores_to_device(s, w)[:, :D]              # strided view
+    d, c, g = _chain_gpu(meta, dm, sd, w.design_seed, meta.gmax)
+    od, est, ec = _chain_oracle(meta, s[:, :D], w.design_seed, meta.gmax)
+    assert np.array_equal(d["mask"].cpu().numpy(), od["mask"])
+    out = g["out"].cpu().numpy()
+    assert np.isfinite(out).all()
+    err = rel_l2(out, est)
+    log(f"  grad rel L2 = {err:.3e}")
+    assert err <= BF16_TOL
+    _assert_zero_rows(meta, c["coeff"], g["out"])
+
+
+def test_weighted_grad_edge_cases():
+    """G = 2 and G = 64 groups, one group above 64 rows, D = 1 and ragged
+    tails, uncompleted rows holding NaN, prompts with fewer than two completed
+    vertices."""
+    rng = np.random.default_rng(99)
+    sizes = [2, 64, 3, 130, 5, 2, 17]
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    nv = int(offsets[-1])
+    for D in (1, 7, 8, 4100):
+        log(f"edge cases D={D}")
+        ld = (D + 7) // 8 * 8                       # 16-byte aligned rows for both dtypes
+        s = rng.standard_normal((nv, D)).astype(np.float32)
+        coeff = rng.standard_normal(nv).astype(np.float32)
+        coeff[rng.random(nv) < 0.4] = 0.0
+        coeff[offsets[2]:offsets[3]] = 0.0          # an all-zero prompt
+        s_nan = np.full((nv, ld), np.nan, dtype=np.float32)
+        s_nan[:, :D] = s
+        s_nan[coeff == 0.0] = np.nan                # never-completed rollouts carry no score
+        off_d = torch.from_numpy(offsets).to(DEV)
+        c_d = torch.from_numpy(coeff).to(DEV)
+        sd = torch.from_numpy(s_nan).to(DEV)[:, :D]
+        out = pair.weighted_grad(off_d, sd, c_d, nv=nv)["out"].cpu().numpy()
+        want = np.stack([coeff[offsets[b]:offsets[b + 1]].astype(np.float64)
+                         @ s[offsets[b]:offsets[b + 1]].astype(np.float64) for b in range(len(sizes))])
+        assert np.isfinite(out).all()
+        assert rel_l2(out, want) <= FP32_TOL
+        assert np.all(out[2] == 0.0)
+        # bf16 path with the same rows
+        sb = torch.from_numpy(s_nan).to(DEV).to(torch.bfloat16)[:, :D]
+        outb = pair.weighted_grad(off_d, sb, c_d, nv=nv)["out"].cpu().numpy()
+        sbf = sb.float().cpu().numpy()
+        sbf[coeff == 0.0] = 0.0
+        wantb = np.stack([coeff[offsets[b]:offsets[b + 1]].astype(np.float64)
+                          @ sbf[offsets[b]:offsets[b + 1]].astype(np.float64)
+                          for b in range(len(sizes))])
+        assert np.isfinite(outb).all() and rel_l2(outb, wantb) <= FP32_TOL
+        assert np.all(outb[2] == 0.0)
+
+
+def test_fewer_than_two_completed_gives_exact_zero():
+    w = wl.WORKLOADS["b128"].replace(B=16, D=512)
+    meta = wl.host_meta(w)
+    meta.p[:] = np.float32(0.02)          # almost every draw completes < 2 vertices
+    log("k<2 zero prompts")
+    dm = upload_meta(meta)
+    s = wl.host_scores(w, meta.nv)
+    d, c, g = _chain_gpu(meta, dm, scores_to_device(s, w), 77, meta.gmax)
+    od, est, _ = _chain_oracle(meta, s, 77, meta.gmax)
+    k = d["completed"].cpu().numpy()[0]
+    assert np.any(k < 2)
+    out = g["out"].cpu().numpy()
+    for b in range(meta.B):
+        if k[b] < 2:
+            assert np.all(out[b] == 0.0)
+    assert rel_l2(out, est) <= BF16_TOL
+
+
+@pytest.mark.parametrize("name,ncols", [("b128", 2048), ("ragged", 1024), ("qwen3", 256)])
+def test_full_size_sampled_columns(name, ncols):
+    """The workload at its full size, in the launch configuration the bench
+    times; the oracle recomputes a random sample of columns (plus the last
+    ones) from the same device-resident scores."""
+    w = wl.WORKLOADS[name]
+    meta = wl.host_meta(w)
+    log(f"full size {name} B={meta.B} nv={meta.nv} D={w.D}")
+    dm = upload_meta(meta)
+    sd = wl.device_scores(w, meta.nv, DEV)
+    d, c, g = _chain_gpu(meta, dm, sd, w.design_seed, meta.gmax)
+    rng = np.random.default_rng(3)
+    cols = np.unique(np.concatenate([rng.choice(w.D, ncols, replace=False), np.arange(w.D - 16, w.D)]))
+    ci = torch.from_numpy(cols).to(DEV)
+    s_host = scores_to_host(sd.index_select(1, ci))
+    out = g["out"].index_select(1, ci).cpu().numpy()
+    od, est, _ = _chain_oracle(meta, s_host, w.design_seed, meta.gmax)
+    assert np.array_equal(d["mask"].cpu().numpy(), od["mask"])
+    err = rel_l2(out, est)
+    log(f"  sampled grad rel L2 = {err:.3e}")
+    assert err <= BF16_TOL
+    _assert_zero_rows(meta, c["coeff"], g["out"])
+    assert torch.isfinite(g["out"]).all()
+    del sd, g
+    torch.cuda.empty_cache()
+
+
+def test_gpu_enumeration_is_design_unbiased():
+    """Theorem 2 on the GPU: all 2^G completion patterns of one population as
+    a batch of prompts; probability-weighted mean of the GPU estimates equals
+    the complete-pair average."""
+    G, D = 8, 300
+    rng = np.random.default_rng(8)
+    r = (rng.random(G) < 0.5).astype(np.float32)
+    r[0], r[1] = 1.0, 0.0
+    p = (rng.integers(8, 65, size=G) / 64.0).astype(np.float32)
+    s = rng.standard_normal((G, D)).astype(np.float32)
+    masks = np.array(list(itertools.product([0, 1], repeat=G)), dtype=np.uint8)
+    n = masks.shape[0]
+    offsets = np.arange(0, (n + 1) * G, G, dtype=np.int64)
+    od = oracle.design_inclusion(np.array([0, G]), p, 1, 0, 1, G)
+    pi = np.repeat(od["pi"], n, axis=0)
+    log("gpu enumeration G=8")
+    off_d = torch.from_numpy(offsets).to(DEV)
+    c = pair.edge_coeffs(off_d, torch.from_numpy(np.tile(r, n)).to(DEV),
+                         torch.from_numpy(masks.reshape(-1)).to(DEV), torch.from_numpy(pi).to(DEV),
+                         G, nv=n * G)
+    g = pair.weighted_grad(off_d, torch.from_numpy(np.tile(s, (n, 1))).to(DEV), c["coeff"],
+                           nv=n * G)["out"].cpu().numpy().astype(np.float64)
+    pd = p.astype(np.float64)
+    probs = np.prod(np.where(masks == 1, pd, 1.0 - pd), axis=1)
+    target, _ = oracle.pair_grad(np.array([0, G]), s, r)
+    assert rel_l2(probs @ g, target[0]) <= FP32_TOL
+
+
+def test_determinism_bitwise():
+    w = wl.WORKLOADS["ragged"].replace(B=64, D=4096)
+    meta = wl.host_meta(w)
+    log("determinism")
+    dm = upload_meta(meta)
+    sd = scores_to_device(wl.host_scores(w, meta.nv), w)
+    a = _chain_gpu(meta, dm, sd, 5, meta.gmax)[2]["out"].clone()
+    b = _chain_gpu(meta, dm, sd, 5, meta.gmax)[2]["out"]
+    assert torch.equal(a, b)
+
+
+def test_status_bits():
+    log("status bits")
+    offsets = torch.tensor([0, 4, 5, 9], dtype=torch.int64, device=DEV)   # G = 4, 1, 4
+    p = torch.full((9,), 0.5, device=DEV)
+    p[6] = 1.5
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    mask = torch.empty((1, 9), dtype=torch.uint8, device=DEV)
+    pair.pair_design_inclusion(3, 9, 4, offsets, p, 1, 0, 1, mask, None, None, None, st)
+    v = int(st.item())
+    assert v & pair.ST_BAD_GROUP and v & pair.ST_P_RANGE
+    # rho = 0 on an observed edge
+    off2 = torch.tensor([0, 3], dtype=torch.int64, device=DEV)
+    pi = torch.zeros((1, 3, 3), dtype=torch.float32, device=DEV)
+    pi[0, 0, 1] = 0.5
+    pi[0, 0, 2] = 0.5
+    st.zero_()
+    coeff = torch.empty(3, device=DEV)
+    pair.pair_edge_coeffs(1, 3, 3, off2, torch.tensor([1.0, 0.0, 1.0], device=DEV),
+                          torch.ones(3, dtype=torch.uint8, device=DEV), pi, coeff, None, st)
+    assert int(st.item()) & pair.ST_RHO_RANGE
+    # the same rho = 0 on an edge that is not observed is legal
+    st.zero_()
+    pair.pair_edge_coeffs(1, 3, 3, off2, torch.tensor([1.0, 0.0, 1.0], device=DEV),
+                          torch.tensor([1, 1, 0], dtype=torch.uint8, device=DEV), pi, coeff, None, st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0 and torch.isfinite(coeff).all()
+
+
+# ------------------------------------------------------------- the audit --
+def _audit_case(w, meta, R, rep0=0, pi_w=None, want_reps=True):
+    dm = upload_meta(meta)
+    ld = (w.D + 7) // 8 * 8                     # 16-byte aligned bf16 rows
+    s = wl.host_scores(w, meta.nv, ld=ld)
+    sd = scores_to_device(s, w)[:, : w.D]
+    s = s[:, : w.D]
+    pw = None if pi_w is None else torch.from_numpy(pi_w).to(DEV)
+    got = pair.audit(dm["offsets"], sd, dm["rewards"], dm["p"], w.design_seed, rep0, R, meta.gmax,
+                     pi_w=pw, want_reps=want_reps, nv=meta.nv)
+    torch.cuda.synchronize()
+    want = oracle.audit(meta.offsets, s, meta.rewards, meta.p, w.design_seed, rep0, R, pi_w=pi_w,
+                        gmax=meta.gmax)
+    return got, want
+
+
+def _check_audit(got, want, label):
+    mse, bias = got["mse"].cpu().numpy(), got["bias_norm"].cpu().numpy()
+    assert int(got["status"].item()) == 0
+    assert np.array_equal(got["edge_count"].cpu().numpy(), want["edge_count"])
+    e_err = rel_l2(got["rep_sqerr"].cpu().numpy(), want["rep_sqerr"])
+    m_err = np.max(np.abs(mse - want["mse"]) / np.maximum(want["mse"], 1e-300))
+    b_err = np.max(np.abs(bias - want["bias_norm"]) / np.maximum(want["bias_norm"], 1e-300))
+    log(f"  {label}: rep_sqerr rel L2 {e_err:.2e}, max mse rel {m_err:.2e}, max bias rel {b_err:.2e}")
+    assert e_err <= BF16_TOL
+    assert m_err <= BF16_TOL
+    assert b_err <= BF16_TOL
+
+
+@pytest.mark.parametrize("name,B,D,R,G", [("audit", 6, 4096 + 40, 300, None),
+                                          ("audit", 3, 1000, 600, 40),
+                                          ("ragged", 12, 777, 130, None),
+                                          ("audit", 2, 512, 2000, 64)])
+def test_audit_reduced_vs_oracle(name, B, D, R, G):
+    w = wl.WORKLOADS[name].replace(B=B, D=D, dtype=wl.BF16)
+    if G:
+        w = w.replace(G=G)
+    meta = wl.host_meta(w)
+    log(f"audit {name} B={B} D={D} R={R} gmax={meta.gmax}")
+    got, want = _audit_case(w, meta, R)
+    _check_audit(got, want, name)
+
+
+def test_audit_unweighted_and_resumable():
+    w = wl.WORKLOADS["audit"].replace(B=4, D=640)
+    meta = wl.host_meta(w)
+    ones = np.ones((meta.B, meta.gmax, meta.gmax), dtype=np.float32)
+    log("audit unweighted (pi_w = 1)")
+    got, want = _audit_case(w, meta, 200, pi_w=ones)
+    _check_audit(got, want, "unweighted")
+    # replicates split over two calls equal one call
+    log("audit resumable")
+    a, _ = _audit_case(w, meta, 100, rep0=0)
+    b, _ = _audit_case(w, meta, 100, rep0=100)
+    both, _ = _audit_case(w, meta, 200, rep0=0)
+    joined = torch.cat([a["rep_sqerr"], b["rep_sqerr"]], dim=1)
+    assert torch.equal(joined, both["rep_sqerr"])
+
+
+def _exact_expected_mse(K, r, p):
+    """Prop. 1 trace, E||g^ - g_pair||^2 under independent Bernoulli vertices,
+    from the Gram matrix K = S S^T (fp64)."""
+    G = r.size
+    M = G * (G - 1) / 2
+    r = r.astype(np.float64)
+    p = p.astype(np.float64)
+
+    def ip(i, j, k, l):      # <h_ij, h_kl>
+        return 0.25 * (r[i] - r[j]) * (r[k] - r[l]) * (K[i, k] - K[i, l] - K[j, k] + K[j, l])
+
+    tot = 0.0
+    for i in range(G):
+        for j in range(i + 1, G):
+            tot += (1.0 / (p[i] * p[j]) - 1.0) * ip(i, j, i, j)
+    for i in range(G):
+        for j in range(G):
+            for k in range(G):
+                if len({i, j, k}) == 3:
+                    tot += (1.0 / p[i] - 1.0) * ip(i, j, i, k)
+    return tot / (M * M)
+
+
+@pytest.mark.timeout(400)
+def test_audit_full_size():
+    """The audit workload at full size (B=256, G=16, D=65536, R=4096): two
+    sampled prompts against the oracle with every replicate, and for all
+    prompts the Monte-Carlo MSE against its exact expectation (Prop. 1)."""
+    w = wl.WORKLOADS["audit"]
+    meta = wl.host_meta(w)
+    log(f"audit full size B={meta.B} D={w.D} R={w.R}")
+    dm = upload_meta(meta)
+    sd = wl.device_scores(w, meta.nv, DEV)
+    got = pair.audit(dm["offsets"], sd, dm["rewards"], dm["p"], w.design_seed, 0, w.R, meta.gmax,
+                     nv=meta.nv)
+    torch.cuda.synchronize()
+    assert int(got["status"].item()) == 0
+    mse = got["mse"].cpu().numpy()
+    reps = got["rep_sqerr"].cpu().numpy().astype(np.float64)
+    assert np.allclose(mse, reps.mean(axis=1), rtol=1e-6, atol=0)
+    # oracle: one prompt with every replicate, a second on a replicate window
+    b = 3
+    o0, o1 = meta.offsets[b], meta.offsets[b + 1]
+    log(f"  oracle prompt {b}, all replicates")
+    want = oracle.audit(np.array([0, o1 - o0]), scores_to_host(sd[o0:o1]), meta.rewards[o0:o1],
+                        meta.p[o0:o1], w.design_seed, 0, w.R, prompt_id=[b])
+    sub = {"mse": got["mse"][b:b + 1], "bias_norm": got["bias_norm"][b:b + 1],
+           "rep_sqerr": got["rep_sqerr"][b:b + 1], "edge_count": got["edge_count"][b:b + 1],
+           "status": got["status"]}
+    _check_audit(sub, want, f"prompt {b}")
+    b, r0, nr = 200, 2048, 256
+    o0, o1 = meta.offsets[b], meta.offsets[b + 1]
+    log(f"  oracle prompt {b}, replicates {r0}..{r0 + nr - 1}")
+    want = oracle.audit(np.array([0, o1 - o0]), scores_to_host(sd[o0:o1]), meta.rewards[o0:o1],
+                        meta.p[o0:o1], w.design_seed, r0, nr, prompt_id=[b])
+    assert np.array_equal(got["edge_count"][b, r0:r0 + nr].cpu().numpy(), want["edge_count"][0])
+    e_err = rel_l2(reps[b, r0:r0 + nr], want["rep_sqerr"][0])
+    log(f"  prompt {b} window: rep_sqerr rel L2 {e_err:.2e}")
+    assert e_err <= BF16_TOL
+    # every prompt: MC MSE within 6 standard errors of the exact expectation
+    S = sd.view(meta.B, 16, w.D).double()
+    K = torch.bmm(S, S.transpose(1, 2).contiguous()).cpu().numpy()
+    z = []
+    for b in range(meta.B):
+        o0, o1 = meta.offsets[b], meta.offsets[b + 1]
+        ex = _exact_expected_mse(K[b], meta.rewards[o0:o1], meta.p[o0:o1])
+        se = reps[b].std(ddof=1) / math.sqrt(w.R)
+        if ex == 0.0:
+            assert mse[b] <= 1e-12
+            continue
+        z.append((mse[b] - ex) / max(se, 1e-30))
+    z = np.array(z)
+    log(f"  MSE z-scores: max |z| = {np.abs(z).max():.2f}, mean z = {z.mean():.3f}")
+    assert np.abs(z).max() < 6.0
+    assert abs(z.mean()) < 6.0 / math.sqrt(len(z)) + 0.5
