@@ -59,6 +59,7 @@ extern "C" {
 #define PAIR_ST_BAD_GROUP 1  /* G_b < 2, G_b > gmax or offsets not monotone    */
 #define PAIR_ST_RHO_RANGE 2  /* an OBSERVED edge has rho outside (0, 1]        */
 #define PAIR_ST_P_RANGE 4    /* a continuation probability outside (0, 1]      */
+#define PAIR_ST_NONFINITE 8  /* a non-finite score in an audited score block    */
 
 /* Largest group size supported by the design draw, the coefficient fold and
  * the audit (one 64-lane wavefront holds one prompt's vertices). */
@@ -152,12 +153,16 @@ size_t pair_audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R)
  *     e_r  = || g_r - t ||^2 = || (A~^(r) - a) S_b ||^2
  *     mse  = (1/R) sum_r e_r
  *     bias = || (1/R) sum_r g_r - t ||
- * The R x D estimates are never materialised: (A~^(r) - a), rounded to bf16,
- * times S_b runs on bf16 matrix cores with the squared norm reduced in the
- * epilogue.  Weights use rho = pi_w when given (e.g. all ones replays the
- * unweighted estimator of Prop. 1), else the logged fl32(p_i p_j).
+ * The R x D estimates are never materialised: (A~^(r) - a) times S_b runs on
+ * the matrix cores with the squared norm reduced in the epilogue.  Operands
+ * are fp16 after exact power-of-two rescaling (score rows by their largest
+ * magnitude, which makes the bf16 -> fp16 conversion exact; each replicate
+ * row of A~^(r) - a by its largest entry, then one fp16 rounding), so e_r
+ * carries a relative error of about 2^-11 per coefficient.  Weights use
+ * rho = pi_w when given (e.g. all ones replays the unweighted estimator of
+ * Prop. 1), else the logged fl32(p_i p_j).
  *
- *   scores, dtype  PAIR_BF16 only (the matrix-core operand type)
+ *   scores, dtype  PAIR_BF16 only, finite values
  *   rewards, p     fp32 [nv]
  *   pi_w           fp32 [B][gmax][gmax] rho used in the weights      (or NULL)
  *   mse, bias_norm fp64 [B] out
@@ -165,7 +170,8 @@ size_t pair_audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R)
  *   edge_count     int32 [B][R] out: observed edges per replicate    (or NULL)
  *   workspace      device scratch of ws_bytes >= pair_audit_workspace_bytes,
  *                  256-byte aligned; contents on entry do not matter
- * Device status: PAIR_ST_BAD_GROUP, PAIR_ST_P_RANGE, PAIR_ST_RHO_RANGE.
+ * Device status: PAIR_ST_BAD_GROUP, PAIR_ST_P_RANGE, PAIR_ST_RHO_RANGE,
+ * PAIR_ST_NONFINITE.
  */
 int pair_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
                const void* scores, int32_t dtype, int64_t ld, const float* rewards,

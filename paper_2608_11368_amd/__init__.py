@@ -28,6 +28,7 @@ PAIR_BF16 = 1
 ST_BAD_GROUP = 1
 ST_RHO_RANGE = 2
 ST_P_RANGE = 4
+ST_NONFINITE = 8
 GMAX_LIMIT = 64
 
 EXPORTED = ("pair_design_inclusion", "pair_edge_coeffs", "pair_weighted_grad",

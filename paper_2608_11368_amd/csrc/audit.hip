@@ -14,18 +14,26 @@
 //                   replicate: Philox draw of J^(r) (same counter reading as
 //                   the design draw), the coefficient fold over a per-prompt
 //                   table W_ij = (r_i - r_j)/rho_ij in LDS, centring over the
-//                   completed vertices, delta_r split into two bf16 terms
-//                   (hi = RNE(delta), lo = RNE(delta - hi)) so the matrix-core
-//                   operand carries ~16 significant bits, and a fixed-order
-//                   fp32 partial sum of delta over the 64 lanes.
-//  2. audit_mean    delta_bar appended as replicate row R, padding rows zeroed.
-//  3. audit_mfma    [rows x 16k] delta (hi and lo terms) times [16k x D] bf16
-//                   S_b on v_mfma_f32_32x32x16_bf16, S_b staged through LDS in a
-//                   transposed layout (one 128-bit LDS read per operand), the
-//                   squared norm of every 32x32 output tile accumulated in the
-//                   epilogue, so the rows x D product is never written.
-//                   Workgroups of one prompt are placed on one XCD so S_b is
-//                   fetched into that XCD's L2 once and reused.
+//                   completed vertices, delta_r stored in fp32, and a
+//                   fixed-order partial sum of delta over the 64 lanes.  The
+//                   same workgroups also scan a slice of S_b for the largest
+//                   magnitude of every score row.
+//  2. audit_prep    delta_bar appended as replicate row R, padding rows
+//                   zeroed, and per-row power-of-two exponents e_i with
+//                   max |s_i| 2^-e_i in [1, 2).
+//  3. audit_mfma    the contraction on v_mfma_f32_32x32x16_f16.  Each score
+//                   row is rescaled by 2^-e_i, which makes the bf16 -> fp16
+//                   conversion exact (8 significant bits fit in 11); each
+//                   replicate row of delta is rescaled by 2^(e_i - f_r), with
+//                   f_r chosen so its largest entry lies in [1, 2), and rounded
+//                   once to fp16 (2^-11 relative).  The products are exact
+//                   rescalings of delta_r S_b, so e_r = 4^f_r * sum of squares.
+//                   S_b is staged through LDS in a transposed layout (one
+//                   128-bit LDS read per operand), the squares of every 32x32
+//                   output tile are accumulated in the epilogue, and the
+//                   rows x D product is never written.  Workgroups of one
+//                   prompt are placed on one XCD so S_b is fetched into that
+//                   XCD's L2 once and reused.
 //  4. audit_finalize fp64 fixed-order MSE, bias = sqrt(e[R]), optional copies.
 #include "common.hpp"
 #include "launch.hpp"
@@ -34,55 +42,73 @@ namespace pair {
 
 namespace {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kCoefThreads = 64;     // replicates per audit_coeffs workgroup
-constexpr int kMfmaThreads = 256;    // 4 waves
-constexpr int kTilesPerWave = 2;     // 32-row MFMA tiles per wave
-constexpr int kRowsPerWave = 32 * kTilesPerWave;
-constexpr int kRowsPerGroup = kRowsPerWave * (kMfmaThreads / kWave);  // 256
-constexpr int kChunk = 256;          // score columns staged per LDS buffer
+constexpr int kScanBytes = 64 << 10; // score bytes scanned per audit_coeffs workgroup (at most)
+constexpr int kMfmaThreads = 512;    // 8 waves per workgroup
+constexpr int kMfmaWaves = kMfmaThreads / kWave;
+constexpr int kTile = 32;            // replicate rows (and score columns) per matrix instruction
+constexpr int kPair = 2;             // replicate tiles a wave carries at once
+
+// Score columns per workgroup slice: the slice of S_b (16 * ks rows, fp16,
+// plus one skew row per 8) stays resident in LDS while all replicate rows
+// sweep over it.
+constexpr int slice_cols(int ks) { return ks == 1 ? 2048 : (ks == 2 ? 1024 : 512); }
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 struct AuditLayout {
   int ks;            // 16-wide K steps (ceil(gmax / 16))
-  int64_t rrows;     // replicate rows per prompt incl. the delta_bar row and padding
-  int64_t groups;    // MFMA workgroups per prompt
-  int64_t nchunk;    // audit_coeffs workgroups per prompt
-  size_t delta_off, e_off, dsum_off, total;
+  int kp;            // 16 * ks: padded K extent
+  int64_t ntiles;    // 32-row replicate tiles per prompt (R rows + the delta_bar row)
+  int64_t rrows;     // ntiles * 32
+  int64_t nslices;   // score-column slices per prompt
+  int64_t nwg;       // audit_coeffs workgroups per prompt
+  int64_t slice;     // score columns scanned per audit_coeffs workgroup
+  size_t delta_off, epart_off, dsum_off, rmax_off, rexp_off, total;
 };
 
-AuditLayout audit_layout(int64_t B, int32_t gmax, int64_t R) {
+AuditLayout audit_layout(int64_t B, int32_t gmax, int64_t D, int64_t R) {
   AuditLayout L;
   L.ks = (gmax + 15) / 16;
-  L.groups = (R + 1 + kRowsPerGroup - 1) / kRowsPerGroup;
-  L.rrows = L.groups * kRowsPerGroup;
-  L.nchunk = (R + kCoefThreads - 1) / kCoefThreads;
+  L.kp = 16 * L.ks;
+  L.ntiles = (R + 1 + kTile - 1) / kTile;
+  L.rrows = L.ntiles * kTile;
+  L.nslices = (D + slice_cols(L.ks) - 1) / slice_cols(L.ks);
+  const int64_t by_reps = (R + kCoefThreads - 1) / kCoefThreads;
+  const int64_t by_scan = ((int64_t)gmax * D * 2 + kScanBytes - 1) / kScanBytes;
+  L.nwg = by_reps > by_scan ? by_reps : by_scan;
+  L.slice = round_up((D + L.nwg - 1) / L.nwg, 8);
   size_t off = 0;
   L.delta_off = off;
-  off += (size_t)round_up((int64_t)B * L.rrows * 2 * 16 * L.ks * 2, 256);  // hi + lo bf16
-  L.e_off = off;
-  off += (size_t)round_up((int64_t)B * L.rrows * 4, 256);
+  off += (size_t)round_up(B * L.rrows * L.kp * 4, 256);            // fp32 delta rows
+  L.epart_off = off;
+  off += (size_t)round_up(B * L.nslices * L.rrows * 4, 256);       // per-slice squared errors
   L.dsum_off = off;
-  off += (size_t)round_up((int64_t)B * L.nchunk * gmax * 4, 256);
+  off += (size_t)round_up(B * L.nwg * gmax * 4, 256);               // partial delta sums
+  L.rmax_off = off;
+  off += (size_t)round_up(B * L.nwg * L.kp * 4, 256);               // partial row maxima
+  L.rexp_off = off;
+  off += (size_t)round_up(B * L.kp * 4, 256);                       // row exponents
   L.total = off;
   return L;
 }
 
 // ---------------------------------------------------------------------------
-// 1. Replicate coefficients.
+// 1. Replicate coefficients (+ row-magnitude scan).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
-    int64_t B, int64_t nv, int32_t gmax, int ks, const int64_t* __restrict__ offsets,
+    int64_t B, int64_t nv, int32_t gmax, int kp, const int64_t* __restrict__ offsets,
     const float* __restrict__ rewards, const float* __restrict__ p,
-    const float* __restrict__ pi_w, uint64_t seed, int64_t rep0, int64_t R, int64_t nchunk,
-    int64_t rrows, uint16_t* __restrict__ delta, float* __restrict__ dsum,
+    const float* __restrict__ pi_w, uint64_t seed, int64_t rep0, int64_t R, int64_t nwg,
+    int64_t rrows, const uint16_t* __restrict__ scores, int64_t ld, int64_t D, int64_t slice,
+    float* __restrict__ delta, float* __restrict__ dsum, uint32_t* __restrict__ rmax,
     int32_t* __restrict__ edge_count, int32_t* d_status) {
   extern __shared__ float lds[];
-  const int64_t b = blockIdx.x / nchunk;
-  const int64_t chunk = blockIdx.x - b * nchunk;
+  const int64_t b = blockIdx.x / nwg;
+  const int64_t chunk = blockIdx.x - b * nwg;
   const int lane = threadIdx.x;
   int64_t o0, g;
   if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, d_status, chunk == 0 && lane == 0)) return;
@@ -93,6 +119,7 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
   float* pl = A + kCoefThreads * stride;  // [gmax]            continuation probabilities
   float* af = pl + gmax;                  // [gmax]            complete-pair coefficients
   float* rl = af + gmax;                  // [gmax]            rewards
+  uint32_t* mx = reinterpret_cast<uint32_t*>(rl + gmax);  // [gmax] row magnitude maxima
 
   const bool vert = lane < g;
   const float r_i = vert ? rewards[o0 + lane] : 0.0f;
@@ -100,6 +127,7 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
   if (vert) {
     pl[lane] = p_i;
     rl[lane] = r_i;
+    mx[lane] = 0u;
     if (!p_in_range(p_i) && chunk == 0) raise_status(d_status, PAIR_ST_P_RANGE);
   }
 
@@ -138,7 +166,45 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
     W[i * stride + j] = w;
   }
   if (bad_rho && chunk == 0) raise_status(d_status, PAIR_ST_RHO_RANGE);
+
+  // Largest |s| of every row over this workgroup's column slice, as bf16
+  // magnitude bits (integer order = magnitude order for finite values).
+  {
+    const int64_t c_lo = chunk * slice;
+    const int64_t c_hi = c_lo + slice < D ? c_lo + slice : D;
+    const int64_t pieces_per_row = c_lo < c_hi ? (c_hi - c_lo + 7) / 8 : 0;
+    const int64_t pieces = g * pieces_per_row;
+    int cur = -1;
+    uint32_t m = 0;
+    for (int64_t q = lane; q < pieces; q += kWave) {
+      const int i = (int)(q / pieces_per_row);
+      const int64_t col = c_lo + 8 * (q - (int64_t)i * pieces_per_row);
+      const uint16_t* src = scores + (o0 + i) * ld + col;
+      if (i != cur) {
+        if (cur >= 0) atomicMax(&mx[cur], m);
+        cur = i;
+        m = 0;
+      }
+      if (col + 8 <= c_hi) {
+        const uint4 v = load_nt16(src);
+        const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t lo = w4[k] & 0x7fffu, hi = (w4[k] >> 16) & 0x7fffu;
+          m = lo > m ? lo : m;
+          m = hi > m ? hi : m;
+        }
+      } else {
+        for (int64_t c = col; c < c_hi; ++c) {
+          const uint32_t h = src[c - col] & 0x7fffu;
+          m = h > m ? h : m;
+        }
+      }
+    }
+    if (cur >= 0) atomicMax(&mx[cur], m);
+  }
   __syncthreads();
+  if (vert) rmax[(b * nwg + chunk) * kp + lane] = mx[lane];
 
   // One replicate per lane.
   const int64_t rloc = chunk * kCoefThreads + lane;
@@ -178,34 +244,26 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
   }
   const float mean = k >= 2 ? sum_obs / (float)k : 0.0f;
 
-  // delta = A~ - a as two bf16 terms [hi x kp | lo x kp]; the fp32 value is
-  // kept for the column sums.
-  const int kp = 16 * ks;
-  uint16_t* drow = delta + ((b * rrows + rloc) * 2 * kp);
-  for (int i0 = 0; i0 < kp; i0 += 8) {
-    uint32_t hi_p[4], lo_p[4];
+  // delta = A~ - a (fp32, zero padded to kp); kept in LDS for the column sums.
+  if (rloc < rrows) {
+    float* drow = delta + (b * rrows + rloc) * kp;
+    for (int i0 = 0; i0 < kp; i0 += 4) {
+      float v4[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      uint16_t h[2], l[2];
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int i = i0 + 2 * q + hh;
+      for (int q = 0; q < 4; ++q) {
+        const int i = i0 + q;
         float dv = 0.0f;
         if (i < g) {
           const float ai = (k >= 2 && ((bits >> i) & 1ull)) ? A[lane * stride + i] - mean : 0.0f;
           dv = valid ? ai - af[i] : 0.0f;
           A[lane * stride + i] = dv;
         }
-        h[hh] = f32_to_bf16_rne(dv);
-        l[hh] = f32_to_bf16_rne(dv - __uint_as_float((uint32_t)h[hh] << 16));
+        v4[q] = dv;
       }
-      hi_p[q] = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
-      lo_p[q] = (uint32_t)l[0] | ((uint32_t)l[1] << 16);
+      if (valid) *reinterpret_cast<float4*>(drow + i0) = make_float4(v4[0], v4[1], v4[2], v4[3]);
     }
-    if (valid) {
-      *reinterpret_cast<uint4*>(drow + i0) = make_uint4(hi_p[0], hi_p[1], hi_p[2], hi_p[3]);
-      *reinterpret_cast<uint4*>(drow + kp + i0) = make_uint4(lo_p[0], lo_p[1], lo_p[2], lo_p[3]);
-    }
+  } else {
+    for (int i = 0; i < g; ++i) A[lane * stride + i] = 0.0f;
   }
   __syncthreads();
 
@@ -213,102 +271,108 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
   if (vert) {
     float s = 0.0f;
     for (int t = 0; t < kCoefThreads; ++t) s += A[t * stride + lane];
-    dsum[(b * nchunk + chunk) * gmax + lane] = s;
+    dsum[(b * nwg + chunk) * gmax + lane] = s;
   }
 }
 
 // ---------------------------------------------------------------------------
-// 2. delta_bar row and zero padding.
+// 2. delta_bar row, zero padding, per-row exponents.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void audit_mean_kernel(int64_t B, int64_t nv, int32_t gmax,
-                                                         int ks, const int64_t* __restrict__ offsets,
-                                                         int64_t R, int64_t nchunk, int64_t rrows,
+__global__ __launch_bounds__(256) void audit_prep_kernel(int64_t B, int64_t nv, int32_t gmax, int kp,
+                                                         const int64_t* __restrict__ offsets,
+                                                         int64_t R, int64_t nwg, int64_t rrows,
                                                          const float* __restrict__ dsum,
-                                                         uint16_t* __restrict__ delta) {
+                                                         const uint32_t* __restrict__ rmax,
+                                                         float* __restrict__ delta,
+                                                         int32_t* __restrict__ rexp,
+                                                         int32_t* d_status) {
   const int64_t b = blockIdx.x;
   int64_t o0, g;
   if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, nullptr, false)) return;
-  const int kp = 16 * ks;
   const int tid = threadIdx.x;
   if (tid < kp) {
     float v = 0.0f;
+    int32_t ex = 0;
     if (tid < g) {
       float s = 0.0f;
-      for (int64_t c = 0; c < nchunk; ++c) s += dsum[(b * nchunk + c) * gmax + tid];
+      uint32_t m = 0;
+      for (int64_t c = 0; c < nwg; ++c) {
+        s += dsum[(b * nwg + c) * gmax + tid];
+        const uint32_t mc = rmax[(b * nwg + c) * kp + tid];
+        m = mc > m ? mc : m;
+      }
       v = s / (float)R;
+      if (m >= 0x7f80u) {                 // inf or NaN in the row
+        raise_status(d_status, PAIR_ST_NONFINITE);
+      } else if (m != 0u) {
+        ex = (int32_t)(m >> 7) - 127;     // 2^ex <= max |s| < 2^(ex+1); -127 for subnormals
+      }
     }
-    const uint16_t hi = f32_to_bf16_rne(v);
-    uint16_t* row = delta + (b * rrows + R) * 2 * kp;
-    row[tid] = hi;
-    row[kp + tid] = f32_to_bf16_rne(v - __uint_as_float((uint32_t)hi << 16));
+    delta[(b * rrows + R) * kp + tid] = v;
+    rexp[b * kp + tid] = ex;
   }
-  const int64_t pad_elems = (rrows - R - 1) * 2 * kp;
-  uint16_t* pad = delta + (b * rrows + R + 1) * 2 * kp;
-  for (int64_t idx = tid; idx < pad_elems; idx += blockDim.x) pad[idx] = 0;
+  const int64_t pad = (rrows - R - 1) * kp;
+  float* dst = delta + (b * rrows + R + 1) * kp;
+  for (int64_t idx = tid; idx < pad; idx += blockDim.x) dst[idx] = 0.0f;
 }
 
 // ---------------------------------------------------------------------------
 // 3. Matrix-core contraction with the squared-norm epilogue.
 //
-// v_mfma_f32_32x32x16_bf16 operand layout (wave64): lane l holds row l % 32
-// of A and column l % 32 of B, with K elements 8*(l/32) .. 8*(l/32)+7.  The
-// 16 accumulator registers of lane l hold column l % 32 and rows
-// 8*(v/4) + 4*(l/32) + (v%4), v = 0..15.  Here A = delta rows (replicates,
-// hi then lo term into the same accumulator), B = S_b^T chunk (columns d), so
-// each accumulator register is one (r, d) entry of delta S_b and its square is
-// added to a per-register running sum.
+// A workgroup owns one prompt and one slice of score columns.  It converts
+// the slice to rescaled fp16 once, keeps it in LDS ([d][i], transposed, one
+// skew row per 8), and then every replicate row of the prompt sweeps over it.
+//
+// v_mfma_f32_32x32x16_f16 (wave64): lane l holds row l % 32 of A and column
+// l % 32 of B, K elements 8*(l/32) .. 8*(l/32)+7 of each 16-wide K step; the
+// 16 accumulators of lane l hold column l % 32 and rows 8*(v/4) + 4*(l/32) +
+// (v%4).  Here A = the S_b slice transposed (rows = score columns d) and
+// B = delta^T (columns = replicates r), so all 16 accumulators of a lane
+// belong to ONE replicate (l % 32): the squared norm is summed inside the
+// lane, and lanes l and l + 32 (the two halves of the d rows) are combined
+// once per tile.  Two accumulator sets alternate between 32-column steps so
+// the matrix instruction of step s issues next to the FMAs squaring step s-1.
 // ---------------------------------------------------------------------------
 template <int KS>
 __global__ __launch_bounds__(kMfmaThreads) void audit_mfma_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets, int64_t D,
-    const uint16_t* __restrict__ scores, int64_t ld, int64_t rrows, int64_t groups,
-    int64_t rows_live, const uint16_t* __restrict__ delta, float* __restrict__ e_out) {
-  constexpr int KP = 16 * KS;                           // padded K
-  constexpr int kPieces = KP * (kChunk / 8);            // 16-byte pieces per chunk
-  constexpr int kPiecesPerThread = kPieces / kMfmaThreads;
-  __shared__ __align__(16) uint16_t S_lds[2][kChunk * KP];  // [d][i] transposed
+    const uint16_t* __restrict__ scores, int64_t ld, int64_t rrows, int64_t ntiles,
+    int64_t nslices, const float* __restrict__ delta, const int32_t* __restrict__ rexp,
+    float* __restrict__ epart) {
+  constexpr int KP = 16 * KS;
+  constexpr int SW = slice_cols(KS);
+  constexpr int kSteps = SW / kTile;
+  constexpr int kRowsLds = SW + SW / 8;
+  __shared__ __align__(16) uint16_t S_lds[kRowsLds * KP];
+  __shared__ float tail_part[kMfmaWaves][kTile];
 
   // XCD-aware placement: hardware round-robins workgroup ids over 8 XCDs;
-  // give each XCD a contiguous range of logical (prompt, row-group) ids.
+  // give each XCD a contiguous range of logical (prompt, slice) ids so the
+  // workgroups of a prompt share that XCD's L2 for the delta rows.
   const int64_t per_xcd = gridDim.x / 8;
   const int64_t L = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (L >= B * groups) return;
-  const int64_t b = L / groups;
-  const int64_t grp = L - b * groups;
+  if (L >= B * nslices) return;
+  const int64_t b = L / nslices;
+  const int64_t sl = L - b * nslices;
   int64_t o0, g;
   if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, nullptr, false)) return;
 
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
   const int lane = tid & (kWave - 1);
-  const int64_t row0 = grp * kRowsPerGroup + wave * kRowsPerWave;
+  const int32_t* ex = rexp + b * KP;
+  const int64_t col0 = sl * (int64_t)SW;
 
-  // A operands: this wave's replicate rows, resident for the whole D loop.
-  // A wave whose rows all lie past the live rows (padding of the last row
-  // group) still stages score chunks for its workgroup but skips the math.
-  const bool wave_live = row0 < rows_live;
-  bf16x8_t Ahi[kTilesPerWave][KS], Alo[kTilesPerWave][KS];
-#pragma unroll
-  for (int t = 0; t < kTilesPerWave; ++t) {
-    const uint16_t* src =
-        delta + (b * rrows + row0 + t * 32 + (lane & 31)) * 2 * KP + 8 * (lane >> 5);
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      Ahi[t][s] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(src + 16 * s));
-      Alo[t][s] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(src + KP + 16 * s));
-    }
-  }
-
-  // Staging map: piece p -> (row i = p % KP, 8-column group p / KP); lanes
-  // with consecutive i write consecutive LDS halfwords.
-  const uint16_t* sb = scores + o0 * ld;
-  uint4 stage[kPiecesPerThread];
-  auto load_chunk = [&](int64_t c0) {
-#pragma unroll
-    for (int q = 0; q < kPiecesPerThread; ++q) {
-      const int pidx = tid + q * kMfmaThreads;
+  // Stage the slice: 16-byte piece p -> row i = p % KP, columns d0 .. d0 + 7
+  // (d0 = 8 (p / KP)); values rescaled by 2^-e_i and converted to fp16
+  // (exact for every value within 2^17 of the row maximum), columns past D
+  // zero-filled.
+  {
+    const uint16_t* sb = scores + o0 * ld;
+    for (int pidx = tid; pidx < KP * (SW / 8); pidx += kMfmaThreads) {
       const int i = pidx % KP;
-      const int64_t col = c0 + 8 * (pidx / KP);
+      const int d0 = 8 * (pidx / KP);
+      const int64_t col = col0 + d0;
       uint4 v = make_uint4(0u, 0u, 0u, 0u);
       if (i < g) {
         const uint16_t* src = sb + (int64_t)i * ld + col;
@@ -324,124 +388,169 @@ __global__ __launch_bounds__(kMfmaThreads) void audit_mfma_kernel(
           v.w = (uint32_t)h[6] | ((uint32_t)h[7] << 16);
         }
       }
-      stage[q] = v;
-    }
-  };
-  auto store_chunk = [&](int buf) {
+      const int ne = -ex[i];
+      const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+      uint16_t* dst = &S_lds[(d0 + d0 / 8) * KP + i];
 #pragma unroll
-    for (int q = 0; q < kPiecesPerThread; ++q) {
-      const int pidx = tid + q * kMfmaThreads;
-      const int i = pidx % KP;
-      const int d0 = 8 * (pidx / KP);
-      uint16_t* dst = &S_lds[buf][d0 * KP + i];
-      const uint4 v = stage[q];
-      dst[0 * KP] = (uint16_t)v.x;
-      dst[1 * KP] = (uint16_t)(v.x >> 16);
-      dst[2 * KP] = (uint16_t)v.y;
-      dst[3 * KP] = (uint16_t)(v.y >> 16);
-      dst[4 * KP] = (uint16_t)v.z;
-      dst[5 * KP] = (uint16_t)(v.z >> 16);
-      dst[6 * KP] = (uint16_t)v.w;
-      dst[7 * KP] = (uint16_t)(v.w >> 16);
+      for (int k = 0; k < 4; ++k) {
+        const float lo = ldexpf(bf16lo_to_f32(w4[k]), ne), hi = ldexpf(bf16hi_to_f32(w4[k]), ne);
+        const uint32_t hpair = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(lo, hi));
+        dst[(2 * k) * KP] = (uint16_t)hpair;
+        dst[(2 * k + 1) * KP] = (uint16_t)(hpair >> 16);
+      }
     }
-  };
-  auto read_b = [&](int buf, int step, bf16x8_t (&Bf)[KS]) {
-    const uint16_t* src = &S_lds[buf][(step * 32 + (lane & 31)) * KP + 8 * (lane >> 5)];
+  }
+  __syncthreads();
+
+  // A fragment (score columns) of step s: lane l reads column 32 s + l % 32 and
+  // the 8 rows 8 (l / 32) .. +7 of every 16-row K step.
+  const int dl = lane & 31;
+  const int aoff = (dl + dl / 8) * KP + 8 * (lane >> 5);
+  auto read_a = [&](int step, f16x8_t (&Af)[KS]) {
+    const uint16_t* src = &S_lds[step * (kTile + kTile / 8) * KP + aoff];
 #pragma unroll
     for (int s = 0; s < KS; ++s)
-      Bf[s] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(src + 16 * s));
+      Af[s] = __builtin_bit_cast(f16x8_t, *reinterpret_cast<const uint4*>(src + 16 * s));
   };
-  auto contract = [&](const bf16x8_t (&Bf)[KS], f32x16_t (&acc)[kTilesPerWave]) {
+  // B fragment (replicate rows) of tile t: lane l holds replicate row
+  // 32 t + l % 32, K entries 16 s + 8 (l / 32) + j, rescaled by 2^(e_i - f_r)
+  // with f_r putting the row's largest entry in [1, 2).
+  auto load_b = [&](int64_t t, f16x8_t (&Bf)[KS], int& f) {
+    const int kh = 8 * (lane >> 5);
+    const float* src = delta + (b * rrows + t * kTile + dl) * KP + kh;
+    float y[KS][8];
+    float m = 0.0f;
 #pragma unroll
-    for (int t = 0; t < kTilesPerWave; ++t) {
-      acc[t] = f32x16_t{};
+    for (int s = 0; s < KS; ++s) {
+      const float4 u0 = *reinterpret_cast<const float4*>(src + 16 * s);
+      const float4 u1 = *reinterpret_cast<const float4*>(src + 16 * s + 4);
+      const float x[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Ahi[t][s], Bf[s], acc[t], 0, 0, 0);
-        acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Alo[t][s], Bf[s], acc[t], 0, 0, 0);
+      for (int j = 0; j < 8; ++j) {
+        y[s][j] = ldexpf(x[j], ex[16 * s + kh + j]);
+        m = fmaxf(m, fabsf(y[s][j]));
       }
     }
+    m = fmaxf(m, __shfl_xor(m, 32, kWave));   // the row's other K half
+    f = m > 0.0f ? ilogbf(m) : 0;
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) Bf[s][j] = (_Float16)ldexpf(y[s][j], -f);
   };
 
-  f32x16_t sq[kTilesPerWave];
+  // Sweep `np` tiles (np <= kPair) over steps [s0, s1); returns each tile's
+  // sum of squares for replicate row l % 32 (lanes l and l + 32 combined).
+  auto sweep = [&](const f16x8_t (&Bt)[kPair][KS], int np, int s0, int s1, float (&out)[kPair]) {
+    f32x16_t accA[kPair], accB[kPair];
+    float sq[kPair][4];
 #pragma unroll
-  for (int t = 0; t < kTilesPerWave; ++t)
+    for (int q = 0; q < kPair; ++q) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) sq[t][v] = 0.0f;
-  auto square_add = [&](const f32x16_t (&acc)[kTilesPerWave]) {
+      for (int v = 0; v < 16; ++v) accB[q][v] = 0.0f;
 #pragma unroll
-    for (int t = 0; t < kTilesPerWave; ++t)
+      for (int k = 0; k < 4; ++k) sq[q][k] = 0.0f;
+    }
+    auto step = [&](const f16x8_t (&Af)[KS], f32x16_t (&acc)[kPair], const f32x16_t (&prev)[kPair]) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) sq[t][v] = __builtin_fmaf(acc[t][v], acc[t][v], sq[t][v]);
-  };
-
-  const int64_t nchunks = (D + kChunk - 1) / kChunk;
-  load_chunk(0);
-  store_chunk(0);
-  __syncthreads();
-  for (int64_t ch = 0; ch < nchunks; ++ch) {
-    const int buf = (int)(ch & 1);
-    const bool more = ch + 1 < nchunks;
-    if (more) load_chunk((ch + 1) * kChunk);
-    if (wave_live) {
-      // Software pipeline: the matrix core works on step s while the vector
-      // ALU squares the outputs of step s - 1.
-      bf16x8_t Bf[KS];
-      f32x16_t accA[kTilesPerWave], accB[kTilesPerWave];
-      read_b(buf, 0, Bf);
-      contract(Bf, accA);
+      for (int q = 0; q < kPair; ++q) {
+        if (q < np) {
+          f32x16_t a;
 #pragma unroll
-      for (int step = 1; step < kChunk / 32; step += 2) {
-        read_b(buf, step, Bf);
-        contract(Bf, accB);
-        square_add(accA);
-        if (step + 1 < kChunk / 32) {
-          read_b(buf, step + 1, Bf);
-          contract(Bf, accA);
+          for (int v = 0; v < 16; ++v) a[v] = 0.0f;
+#pragma unroll
+          for (int s = 0; s < KS; ++s)
+            a = __builtin_amdgcn_mfma_f32_32x32x16_f16(Af[s], Bt[q][s], a, 0, 0, 0);
+          acc[q] = a;
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            sq[q][v & 3] = __builtin_fmaf(prev[q][v], prev[q][v], sq[q][v & 3]);
+          __builtin_amdgcn_sched_group_barrier(0x008, KS, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
         }
-        square_add(accB);
       }
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    f16x8_t A0[KS], A1[KS];
+    int st = s0;
+    if (st < s1) read_a(st, A0);
+    for (; st + 1 < s1; st += 2) {
+      read_a(st + 1, A1);
+      step(A0, accA, accB);
+      if (st + 2 < s1) read_a(st + 2, A0);
+      step(A1, accB, accA);
     }
-    if (more) store_chunk(buf ^ 1);
-    __syncthreads();
-  }
+    if (st < s1) {            // odd step count: one more step into accA
+      step(A0, accA, accB);
+#pragma unroll
+      for (int q = 0; q < kPair; ++q)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) accB[q][v] = accA[q][v];
+    }
+#pragma unroll
+    for (int q = 0; q < kPair; ++q) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sq[q][v & 3] = __builtin_fmaf(accB[q][v], accB[q][v], sq[q][v & 3]);
+      float tot = (sq[q][0] + sq[q][1]) + (sq[q][2] + sq[q][3]);
+      tot += __shfl_xor(tot, 32, kWave);
+      out[q] = tot;
+    }
+  };
 
-  // Sum each register over the 32 lanes that share its rows (xor over lane
-  // bits 0..4), then lane l (l % 32 < 16) writes register v = l % 32.
+  float* eo = epart + (b * nslices + sl) * rrows;
+  // Main tiles in pairs, round-robin over the waves; the tiles left over
+  // (fewer than one pair per wave) are split by steps across all waves.
+  const int64_t per_round = (int64_t)kPair * kMfmaWaves;
+  const int64_t nmain = ntiles / per_round * per_round;
+  for (int64_t t0 = (int64_t)wave * kPair; t0 < nmain; t0 += per_round) {
+    f16x8_t Bt[kPair][KS];
+    int fr[kPair];
 #pragma unroll
-  for (int t = 0; t < kTilesPerWave; ++t) {
-    float mine = 0.0f;
+    for (int q = 0; q < kPair; ++q) load_b(t0 + q, Bt[q], fr[q]);
+    float out[kPair];
+    sweep(Bt, kPair, 0, kSteps, out);
+    if (lane < kTile) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      float x = sq[t][v];
-#pragma unroll
-      for (int m = 1; m < 32; m <<= 1) x += __shfl_xor(x, m, kWave);
-      if ((lane & 31) == v) mine = x;
+      for (int q = 0; q < kPair; ++q) eo[(t0 + q) * kTile + lane] = ldexpf(out[q], 2 * fr[q]);
     }
-    const int v = lane & 31;
-    if (v < 16) {
-      const int64_t row = row0 + t * 32 + 8 * (v / 4) + 4 * (lane >> 5) + (v % 4);
-      e_out[b * rrows + row] = mine;
+  }
+  for (int64_t t = nmain; t < ntiles; ++t) {
+    f16x8_t Bt[kPair][KS];
+    int fr[kPair];
+    load_b(t, Bt[0], fr[0]);
+    const int s0 = wave * kSteps / kMfmaWaves, s1 = (wave + 1) * kSteps / kMfmaWaves;
+    float out[kPair];
+    sweep(Bt, 1, s0, s1, out);
+    if (lane < kTile) tail_part[wave][lane] = out[0];
+    __syncthreads();
+    if (wave == 0 && lane < kTile) {
+      float tot = 0.0f;
+      for (int w = 0; w < kMfmaWaves; ++w) tot += tail_part[w][lane];
+      eo[t * kTile + lane] = ldexpf(tot, 2 * fr[0]);
     }
+    __syncthreads();
   }
 }
 
 // ---------------------------------------------------------------------------
-// 4. Fixed-order fp64 reductions.
+// 4. Fixed-order reductions: e_r = sum over slices (fp32, slice order), then
+//    MSE = mean_r e_r (fp64) and bias = sqrt(e_R).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void audit_finalize_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets, int64_t R,
-    int64_t rrows, const float* __restrict__ e, double* __restrict__ mse,
+    int64_t rrows, int64_t nslices, const float* __restrict__ epart, double* __restrict__ mse,
     double* __restrict__ bias_norm, float* __restrict__ rep_sqerr) {
   __shared__ double part[256];
   const int64_t b = blockIdx.x;
   int64_t o0, g;
   if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, nullptr, false)) return;
-  const float* eb = e + b * rrows;
+  const float* eb = epart + b * nslices * rrows;
   double s = 0.0;
   for (int64_t r = threadIdx.x; r < R; r += blockDim.x) {
-    s += (double)eb[r];
-    if (rep_sqerr != nullptr) rep_sqerr[b * R + r] = eb[r];
+    float e = 0.0f;
+    for (int64_t k = 0; k < nslices; ++k) e += eb[k * rrows + r];
+    s += (double)e;
+    if (rep_sqerr != nullptr) rep_sqerr[b * R + r] = e;
   }
   part[threadIdx.x] = s;
   __syncthreads();
@@ -450,16 +559,17 @@ __global__ __launch_bounds__(256) void audit_finalize_kernel(
     __syncthreads();
   }
   if (threadIdx.x == 0) {
+    float eR = 0.0f;
+    for (int64_t k = 0; k < nslices; ++k) eR += eb[k * rrows + R];
     mse[b] = part[0] / (double)R;
-    bias_norm[b] = sqrt((double)eb[R]);
+    bias_norm[b] = sqrt((double)eR);
   }
 }
 
 }  // namespace
 
 size_t audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R) {
-  (void)D;
-  return audit_layout(B, gmax, R).total;
+  return audit_layout(B, gmax, D, R).total;
 }
 
 int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
@@ -467,53 +577,45 @@ int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, in
                  const float* pi_w, uint64_t seed, int64_t rep0, int64_t R, double* mse,
                  double* bias_norm, float* rep_sqerr, int32_t* edge_count, void* workspace,
                  int32_t* d_status, hipStream_t stream) {
-  const AuditLayout L = audit_layout(B, gmax, R);
+  const AuditLayout L = audit_layout(B, gmax, D, R);
   unsigned char* ws = static_cast<unsigned char*>(workspace);
-  uint16_t* delta = reinterpret_cast<uint16_t*>(ws + L.delta_off);
-  float* e = reinterpret_cast<float*>(ws + L.e_off);
+  float* delta = reinterpret_cast<float*>(ws + L.delta_off);
+  float* epart = reinterpret_cast<float*>(ws + L.epart_off);
   float* dsum = reinterpret_cast<float*>(ws + L.dsum_off);
-
-  const int64_t coef_grid = B * L.nchunk;
-  if (coef_grid > 0x7fffffffLL) return PAIR_ERANGE;
-  const size_t coef_lds =
-      ((size_t)gmax * (gmax + 1) + (size_t)kCoefThreads * (gmax + 1) + 3 * (size_t)gmax) *
-      sizeof(float);
-  hipLaunchKernelGGL(audit_coeffs_kernel, dim3((unsigned)coef_grid), dim3(kCoefThreads), coef_lds,
-                     stream, B, nv, gmax, L.ks, offsets, rewards, p, pi_w, seed, rep0, R,
-                     L.nchunk, L.rrows, delta, dsum, edge_count, d_status);
-  if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
-
-  hipLaunchKernelGGL(audit_mean_kernel, dim3((unsigned)B), dim3(256), 0, stream, B, nv, gmax,
-                     L.ks, offsets, R, L.nchunk, L.rrows, dsum, delta);
-  if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
-
-  const int64_t logical = B * L.groups;
-  const int64_t grid = round_up(logical, 8);
-  if (grid > 0x7fffffffLL) return PAIR_ERANGE;
+  uint32_t* rmax = reinterpret_cast<uint32_t*>(ws + L.rmax_off);
+  int32_t* rexp = reinterpret_cast<int32_t*>(ws + L.rexp_off);
   const uint16_t* s = static_cast<const uint16_t*>(scores);
-  const int64_t rows_live = R + 1;
+
+  const int64_t coef_grid = B * L.nwg;
+  if (coef_grid > 0x7fffffffLL) return PAIR_ERANGE;
+  const size_t coef_lds = ((size_t)gmax * (gmax + 1) + (size_t)kCoefThreads * (gmax + 1) +
+                           4 * (size_t)gmax) * sizeof(float);
+  hipLaunchKernelGGL(audit_coeffs_kernel, dim3((unsigned)coef_grid), dim3(kCoefThreads), coef_lds,
+                     stream, B, nv, gmax, L.kp, offsets, rewards, p, pi_w, seed, rep0, R, L.nwg,
+                     L.rrows, s, ld, D, L.slice, delta, dsum, rmax, edge_count, d_status);
+  if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
+
+  hipLaunchKernelGGL(audit_prep_kernel, dim3((unsigned)B), dim3(256), 0, stream, B, nv, gmax, L.kp,
+                     offsets, R, L.nwg, L.rrows, dsum, rmax, delta, rexp, d_status);
+  if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
+
+  const int64_t grid = round_up(B * L.nslices, 8);
+  if (grid > 0x7fffffffLL) return PAIR_ERANGE;
+#define PAIR_AUDIT_MFMA(KS_)                                                                   \
+  hipLaunchKernelGGL(audit_mfma_kernel<KS_>, dim3((unsigned)grid), dim3(kMfmaThreads), 0, stream, \
+                     B, nv, gmax, offsets, D, s, ld, L.rrows, L.ntiles, L.nslices, delta, rexp,  \
+                     epart)
   switch (L.ks) {
-    case 1:
-      hipLaunchKernelGGL(audit_mfma_kernel<1>, dim3((unsigned)grid), dim3(kMfmaThreads), 0, stream,
-                         B, nv, gmax, offsets, D, s, ld, L.rrows, L.groups, rows_live, delta, e);
-      break;
-    case 2:
-      hipLaunchKernelGGL(audit_mfma_kernel<2>, dim3((unsigned)grid), dim3(kMfmaThreads), 0, stream,
-                         B, nv, gmax, offsets, D, s, ld, L.rrows, L.groups, rows_live, delta, e);
-      break;
-    case 3:
-      hipLaunchKernelGGL(audit_mfma_kernel<3>, dim3((unsigned)grid), dim3(kMfmaThreads), 0, stream,
-                         B, nv, gmax, offsets, D, s, ld, L.rrows, L.groups, rows_live, delta, e);
-      break;
-    default:
-      hipLaunchKernelGGL(audit_mfma_kernel<4>, dim3((unsigned)grid), dim3(kMfmaThreads), 0, stream,
-                         B, nv, gmax, offsets, D, s, ld, L.rrows, L.groups, rows_live, delta, e);
-      break;
+    case 1: PAIR_AUDIT_MFMA(1); break;
+    case 2: PAIR_AUDIT_MFMA(2); break;
+    case 3: PAIR_AUDIT_MFMA(3); break;
+    default: PAIR_AUDIT_MFMA(4); break;
   }
+#undef PAIR_AUDIT_MFMA
   if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
 
   hipLaunchKernelGGL(audit_finalize_kernel, dim3((unsigned)B), dim3(256), 0, stream, B, nv, gmax,
-                     offsets, R, L.rrows, e, mse, bias_norm, rep_sqerr);
+                     offsets, R, L.rrows, L.nslices, epart, mse, bias_norm, rep_sqerr);
   return hipGetLastError() == hipSuccess ? PAIR_OK : PAIR_EHIP;
 }
 
