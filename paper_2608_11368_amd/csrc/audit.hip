@@ -334,7 +334,7 @@ __global__ __launch_bounds__(256) void audit_prep_kernel(int64_t B, int64_t nv, 
 // the matrix instruction of step s issues next to the FMAs squaring step s-1.
 // ---------------------------------------------------------------------------
 template <int KS>
-__global__ __launch_bounds__(kMfmaThreads) void audit_mfma_kernel(
+__global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS == 1 ? 4 : 2))) void audit_mfma_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets, int64_t D,
     const uint16_t* __restrict__ scores, int64_t ld, int64_t rrows, int64_t ntiles,
     int64_t nslices, const float* __restrict__ delta, const int32_t* __restrict__ rexp,
