@@ -28,13 +28,15 @@
 //                   f_r chosen so its largest entry lies in [1, 2), and rounded
 //                   once to fp16 (2^-11 relative).  The products are exact
 //                   rescalings of delta_r S_b, so e_r = 4^f_r * sum of squares.
-//                   S_b is staged through LDS in a transposed layout (one
-//                   128-bit LDS read per operand), the squares of every 32x32
-//                   output tile are accumulated in the epilogue, and the
-//                   rows x D product is never written.  Workgroups of one
-//                   prompt are placed on one XCD so S_b is fetched into that
-//                   XCD's L2 once and reused.
-//  4. audit_finalize fp64 fixed-order MSE, bias = sqrt(e[R]), optional copies.
+//                   A workgroup owns one prompt and one slice of score
+//                   columns: the slice is converted once into LDS and every
+//                   replicate row sweeps over it, so S_b is read from HBM
+//                   once; the squares of every output tile are summed in the
+//                   epilogue and the rows x D product is never written.
+//                   Workgroups of one prompt are placed on one XCD so its
+//                   delta rows are shared through that XCD's L2.
+//  4. audit_finalize per-slice partial sums reduced in fixed order, then
+//                   fp64 MSE, bias = sqrt(e[R]), optional copies.
 #include "common.hpp"
 #include "launch.hpp"
 
