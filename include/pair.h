@@ -121,20 +121,26 @@ int pair_edge_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets
 /*
  * pair_weighted_grad -- the induced-edge HT gradient, paper Eq. (pair-ht)
  * written as sum_i A~_i s_i (Sec. 3.5), batched over prompts:
- *     out[b][d] = sum_{i < G_b} coeff[offsets[b] + i] * s[offsets[b] + i][d]
- * with fp32 accumulation in a fixed order.  Rows whose coefficient is exactly
- * zero (unobserved rollouts, saturated prompts) are neither read nor summed:
- * an uncompleted rollout has no score, so its row may hold anything.
+ *     reduce = 0:  out[b][d] = sum_{i < G_b} coeff[offsets[b] + i] * s[offsets[b] + i][d]
+ *     reduce = 1:  out[d]    = (1/B) sum_b (the same per-prompt sum),
+ * i.e. the batch mean of the per-prompt estimates, summed flat over the packed
+ * rows offsets[0] .. offsets[B]-1.  fp32 accumulation in a fixed order.  Rows
+ * whose coefficient is exactly zero (unobserved rollouts, saturated prompts)
+ * are neither read nor summed: an uncompleted rollout has no score, so its
+ * row may hold anything.
  *
  *   D, scores, dtype, ld   score block (PAIR_F32 or PAIR_BF16), row stride ld
  *   coeff          fp32 [nv] (from pair_edge_coeffs)
- *   out            fp32 [B][D] out (rows packed with stride D)
- * Any G_b >= 0 is accepted here.  Device status: PAIR_ST_BAD_GROUP
- * (offsets not monotone or beyond nv: that prompt's row is not written).
+ *   out            fp32 [B][D] (reduce = 0, rows packed with stride D) or
+ *                  fp32 [D] (reduce = 1) out
+ *   reduce         0 or 1 (anything else: PAIR_EINVAL)
+ * Any G_b >= 0 is accepted here.  Device status: PAIR_ST_BAD_GROUP (offsets
+ * not monotone or beyond nv: with reduce = 0 that prompt's row is not
+ * written; with reduce = 1 the output is unspecified).
  */
 int pair_weighted_grad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D,
                        const void* scores, int32_t dtype, int64_t ld, const float* coeff,
-                       float* out, int32_t* d_status, void* stream);
+                       float* out, int32_t reduce, int32_t* d_status, void* stream);
 
 /*
  * pair_audit_workspace_bytes -- device workspace that pair_audit needs for

@@ -58,7 +58,7 @@ def lib() -> ctypes.CDLL:
         L.pair_design_inclusion.restype = ctypes.c_int
         L.pair_edge_coeffs.argtypes = [i64, i64, i32, P, P, P, P, P, P, P, P]
         L.pair_edge_coeffs.restype = ctypes.c_int
-        L.pair_weighted_grad.argtypes = [i64, i64, P, i64, P, i32, i64, P, P, P, P]
+        L.pair_weighted_grad.argtypes = [i64, i64, P, i64, P, i32, i64, P, P, i32, P, P]
         L.pair_weighted_grad.restype = ctypes.c_int
         L.pair_audit_workspace_bytes.argtypes = [i64, i32, i64, i64]
         L.pair_audit_workspace_bytes.restype = ctypes.c_size_t
@@ -146,11 +146,12 @@ def pair_edge_coeffs(B, nv, gmax, offsets, rewards, mask, pi, coeff, edge_count=
         _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_edge_coeffs")
 
 
-def pair_weighted_grad(B, nv, offsets, scores, coeff, out, d_status=None, stream=None):
+def pair_weighted_grad(B, nv, offsets, scores, coeff, out, reduce=0, d_status=None, stream=None):
     sp, code, ld, D = _scores_arg(scores)
     _rc(lib().pair_weighted_grad(
         B, nv, _dev(offsets, "offsets", torch.int64, B + 1), D, sp, code, ld,
-        _dev(coeff, "coeff", torch.float32, nv), _dev(out, "out", torch.float32, B * D),
+        _dev(coeff, "coeff", torch.float32, nv),
+        _dev(out, "out", torch.float32, D if reduce else B * D), int(reduce),
         _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_weighted_grad")
 
 
@@ -207,13 +208,14 @@ def edge_coeffs(offsets, rewards, mask, pi, gmax, nv=None, stream=None):
     return {"coeff": coeff, "edge_count": ec, "status": st}
 
 
-def weighted_grad(offsets, scores, coeff, nv=None, stream=None):
+def weighted_grad(offsets, scores, coeff, nv=None, reduce=False, stream=None):
     B = offsets.numel() - 1
     nv = _nv(offsets) if nv is None else nv
     D = scores.shape[1]
-    out = torch.empty((B, D), dtype=torch.float32, device=scores.device)
+    shape = (D,) if reduce else (B, D)
+    out = torch.empty(shape, dtype=torch.float32, device=scores.device)
     st = torch.zeros(1, dtype=torch.int32, device=scores.device)
-    pair_weighted_grad(B, nv, offsets, scores, coeff, out, st, stream)
+    pair_weighted_grad(B, nv, offsets, scores, coeff, out, int(bool(reduce)), st, stream)
     return {"out": out, "status": st}
 
 

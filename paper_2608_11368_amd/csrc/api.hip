@@ -84,13 +84,14 @@ int pair_edge_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets
 
 int pair_weighted_grad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D,
                        const void* scores, int32_t dtype, int64_t ld, const float* coeff,
-                       float* out, int32_t* d_status, void* stream) {
+                       float* out, int32_t reduce, int32_t* d_status, void* stream) {
   if (offsets == nullptr || coeff == nullptr || out == nullptr) return PAIR_EINVAL;
+  if (reduce != 0 && reduce != 1) return PAIR_EINVAL;
   if (B < 1 || B > 0x7fffffffLL || nv < 0 || nv > kMaxCount) return PAIR_EINVAL;
   int st = check_scores(scores, dtype, D, ld);
   if (st) return st;
   if (B > kMaxCount / D) return PAIR_ERANGE;
-  return pair::launch_wgrad(B, nv, offsets, D, scores, dtype, ld, coeff, out, d_status,
+  return pair::launch_wgrad(B, nv, offsets, D, scores, dtype, ld, coeff, out, reduce, d_status,
                             as_stream(stream));
 }
 

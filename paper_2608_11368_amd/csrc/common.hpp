@@ -58,6 +58,7 @@ __device__ __forceinline__ bool p_in_range(float p) { return p > 0.0f && p <= 1.
 
 // Non-temporal 16-byte global accesses for data streamed exactly once.
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint4 load_nt16(const void* src) {

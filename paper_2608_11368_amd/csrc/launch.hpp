@@ -20,8 +20,8 @@ int launch_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                   int32_t* edge_count, int32_t* d_status, hipStream_t stream);
 
 int launch_wgrad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D, const void* scores,
-                 int32_t dtype, int64_t ld, const float* coeff, float* out, int32_t* d_status,
-                 hipStream_t stream);
+                 int32_t dtype, int64_t ld, const float* coeff, float* out, int32_t reduce,
+                 int32_t* d_status, hipStream_t stream);
 
 size_t audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R);
 

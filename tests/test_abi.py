@@ -81,13 +81,15 @@ def test_edge_coeffs_rejects_bad_arguments():
 def test_weighted_grad_rejects_bad_arguments():
     f = pair.lib().pair_weighted_grad
 
-    def call(B=4, nv=32, off=FAKE, D=64, s=FAKE, dt=1, ld=64, c=FAKE, out=FAKE):
-        return f(B, nv, off, D, s, dt, ld, c, out, NULL, NULL)
+    def call(B=4, nv=32, off=FAKE, D=64, s=FAKE, dt=1, ld=64, c=FAKE, out=FAKE, reduce=0):
+        return f(B, nv, off, D, s, dt, ld, c, out, reduce, NULL, NULL)
 
     assert call(off=NULL) == -1
     assert call(s=NULL) == -1
     assert call(c=NULL) == -1
     assert call(out=NULL) == -1
+    assert call(reduce=2) == -1
+    assert call(reduce=-1) == -1
     assert call(dt=7) == -2
     assert call(D=0) == -3
     assert call(ld=63) == -3

@@ -1,13 +1,14 @@
 """GPU parity: the HIP path, called through the C ABI, against the CPU oracle.
 
-Bars (stated by the task for this estimator):
+Bars:
   - masks, completed counts, edge counts, logged rho: bit-exact
   - gradients / coefficients: relative L2 <= 1e-5 for fp32 scores,
     <= 2e-3 for bf16 scores (fp32 accumulation on the GPU, fp64 in the oracle)
   - prompts whose estimate is exactly zero (saturated rewards, < 2 completed
     vertices) are exactly zero on the GPU
   - audit: per-replicate squared errors, MSE and bias norm within 2e-3
-    relative (bf16 matrix-core operands), edge counts bit-exact
+    relative (fp16 matrix-core operands after power-of-two scaling), edge
+    counts bit-exact
 Full-size workloads are checked on sampled columns / prompts, plus
 properties that hold at any size.
 """
@@ -227,6 +228,106 @@ def test_full_size_sampled_columns(name, ncols):
     torch.cuda.empty_cache()
 
 
+# ------------------------------------------- weighted gradient, batch mean --
+def test_weighted_grad_mean_tiny_fp32():
+    w = wl.WORKLOADS["tiny"]
+    meta = wl.host_meta(w)
+    log("batch mean tiny fp32")
+    dm = upload_meta(meta)
+    s = wl.host_scores(w, meta.nv)
+    d = pair.design_inclusion(dm["offsets"], dm["p"], w.design_seed, 0, 1, meta.gmax, nv=meta.nv)
+    c = pair.edge_coeffs(dm["offsets"], dm["rewards"], d["mask"][0], d["pi"], meta.gmax,
+                         nv=meta.nv)
+    g = pair.weighted_grad(dm["offsets"], scores_to_device(s, w), c["coeff"], nv=meta.nv,
+                           reduce=True)
+    torch.cuda.synchronize()
+    _, est, _ = _chain_oracle(meta, s, w.design_seed, meta.gmax)
+    err = rel_l2(g["out"].cpu().numpy(), est.mean(axis=0))
+    log(f"  mean rel L2 = {err:.3e}")
+    assert g["out"].shape == (w.D,) and err <= FP32_TOL
+    assert int(g["status"].item()) == 0
+
+
+@pytest.mark.parametrize("name,B,D,pad", [("b128", 32, 4096 + 37, 24), ("ragged", 96, 2048 + 13, 8),
+                                          ("qwen3", 16, 1024, 0)])
+def test_weighted_grad_mean_bf16_reduced(name, B, D, pad):
+    w = wl.WORKLOADS[name].replace(B=B, D=D)
+    meta = wl.host_meta(w)
+    ld = (D + 7) // 8 * 8 + pad
+    log(f"batch mean {name} B={B} D={D} ld={ld}")
+    dm = upload_meta(meta)
+    s = wl.host_scores(w, meta.nv, ld=ld)           # NaN in the row padding
+    sd = scores_to_device(s, w)[:, :D]
+    d, c, _ = _chain_gpu(meta, dm, sd, w.design_seed, meta.gmax)
+    gm = pair.weighted_grad(dm["offsets"], sd, c["coeff"], nv=meta.nv, reduce=True)
+    torch.cuda.synchronize()
+    _, est, _ = _chain_oracle(meta, s[:, :D], w.design_seed, meta.gmax)
+    out = gm["out"].cpu().numpy()
+    assert np.isfinite(out).all()
+    err = rel_l2(out, est.mean(axis=0))
+    log(f"  mean rel L2 = {err:.3e}")
+    assert err <= BF16_TOL
+
+
+def test_weighted_grad_mean_edge_cases():
+    """Groups above 64 rows, D = 1 and ragged tails, NaN in every row with a
+    zero coefficient, and an all-zero batch (exactly zero output)."""
+    rng = np.random.default_rng(7)
+    sizes = [2, 64, 3, 130, 5, 2, 17]
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    nv = int(offsets[-1])
+    off_d = torch.from_numpy(offsets).to(DEV)
+    for D in (1, 7, 8, 1029, 4100):
+        log(f"batch mean edge cases D={D}")
+        ld = (D + 7) // 8 * 8
+        s = rng.standard_normal((nv, D)).astype(np.float32)
+        coeff = rng.standard_normal(nv).astype(np.float32)
+        coeff[rng.random(nv) < 0.4] = 0.0
+        s_nan = np.full((nv, ld), np.nan, dtype=np.float32)
+        s_nan[:, :D] = s
+        s_nan[coeff == 0.0] = np.nan
+        want = (coeff.astype(np.float64) @ s.astype(np.float64)) / len(sizes)
+        sd = torch.from_numpy(s_nan).to(DEV)[:, :D]
+        out = pair.weighted_grad(off_d, sd, torch.from_numpy(coeff).to(DEV), nv=nv,
+                                 reduce=True)["out"].cpu().numpy()
+        assert np.isfinite(out).all() and rel_l2(out, want) <= FP32_TOL
+        sb = torch.from_numpy(s_nan).to(DEV).to(torch.bfloat16)[:, :D]
+        sbf = sb.float().cpu().numpy()
+        sbf[coeff == 0.0] = 0.0
+        wantb = (coeff.astype(np.float64) @ sbf[:, :D].astype(np.float64)) / len(sizes)
+        outb = pair.weighted_grad(off_d, sb, torch.from_numpy(coeff).to(DEV), nv=nv,
+                                  reduce=True)["out"].cpu().numpy()
+        assert np.isfinite(outb).all() and rel_l2(outb, wantb) <= FP32_TOL
+        zero = pair.weighted_grad(off_d, sd, torch.zeros(nv, device=DEV), nv=nv,
+                                  reduce=True)["out"]
+        assert bool((zero == 0).all())
+
+
+def test_weighted_grad_mean_full_size_sampled():
+    """b128 at full size in batch-mean mode, sampled columns against the oracle."""
+    w = wl.WORKLOADS["b128"]
+    meta = wl.host_meta(w)
+    log(f"batch mean full size b128 nv={meta.nv} D={w.D}")
+    dm = upload_meta(meta)
+    sd = wl.device_scores(w, meta.nv, DEV)
+    d, c, g = _chain_gpu(meta, dm, sd, w.design_seed, meta.gmax)
+    gm = pair.weighted_grad(dm["offsets"], sd, c["coeff"], nv=meta.nv, reduce=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(5)
+    cols = np.unique(np.concatenate([rng.choice(w.D, 2048, replace=False),
+                                     np.arange(w.D - 16, w.D)]))
+    ci = torch.from_numpy(cols).to(DEV)
+    s_host = scores_to_host(sd.index_select(1, ci))
+    _, est, _ = _chain_oracle(meta, s_host, w.design_seed, meta.gmax)
+    err = rel_l2(gm["out"].index_select(0, ci).cpu().numpy(), est.mean(axis=0))
+    log(f"  sampled mean rel L2 = {err:.3e}")
+    assert err <= BF16_TOL
+    # the batch mean of the per-prompt rows, on every column (fp32 rounding only)
+    assert rel_l2(gm["out"].double().cpu().numpy(), g["out"].double().mean(0).cpu().numpy()) <= 1e-6
+    del sd, g, gm
+    torch.cuda.empty_cache()
+
+
 def test_gpu_enumeration_is_design_unbiased():
     """Theorem 2 on the GPU: all 2^G completion patterns of one population as
     a batch of prompts; probability-weighted mean of the GPU estimates equals
@@ -292,6 +393,16 @@ def test_status_bits():
                           torch.tensor([1, 1, 0], dtype=torch.uint8, device=DEV), pi, coeff, None, st)
     torch.cuda.synchronize()
     assert int(st.item()) == 0 and torch.isfinite(coeff).all()
+    # batch mean: offsets not monotone, then offsets beyond nv (nothing is read)
+    sc = torch.zeros((9, 8), dtype=torch.float32, device=DEV)
+    c9 = torch.ones(9, device=DEV)
+    gm = torch.empty(8, device=DEV)
+    for bad in ([0, 5, 3, 9], [0, 4, 12]):
+        st.zero_()
+        ob = torch.tensor(bad, dtype=torch.int64, device=DEV)
+        pair.pair_weighted_grad(len(bad) - 1, 9, ob, sc, c9, gm, 1, st)
+        torch.cuda.synchronize()
+        assert int(st.item()) & pair.ST_BAD_GROUP
 
 
 # ------------------------------------------------------------- the audit --
