@@ -15,15 +15,14 @@
 //                   the design draw), the coefficient fold over a per-prompt
 //                   table W_ij = (r_i - r_j)/rho_ij in LDS, centring over the
 //                   completed vertices, delta_r stored in fp32, and a
-//                   fixed-order partial sum of delta over the 64 lanes.  The
-//                   same workgroups also scan a slice of S_b for the largest
-//                   magnitude of every score row.
+//                   fixed-order partial sum of delta over the 64 lanes.
 //  2. audit_prep    delta_bar appended as replicate row R, padding rows
-//                   zeroed, and per-row power-of-two exponents e_i with
-//                   max |s_i| 2^-e_i in [1, 2).
+//                   zeroed.
 //  3. audit_mfma    the contraction on v_mfma_f32_32x32x16_f16.  Each score
-//                   row is rescaled by 2^-e_i, which makes the bf16 -> fp16
-//                   conversion exact (8 significant bits fit in 11); each
+//                   row of a column slice is rescaled by 2^-e_i, with e_i
+//                   the exponent of the row's largest magnitude within the
+//                   slice, which makes the bf16 -> fp16 conversion exact
+//                   (8 significant bits fit in 11); each
 //                   replicate row of delta is rescaled by 2^(e_i - f_r), with
 //                   f_r chosen so its largest entry lies in [1, 2), and rounded
 //                   once to fp16 (2^-11 relative).  The products are exact
@@ -35,8 +34,9 @@
 //                   epilogue and the rows x D product is never written.
 //                   Workgroups of one prompt are placed on one XCD so its
 //                   delta rows are shared through that XCD's L2.
-//  4. audit_finalize per-slice partial sums reduced in fixed order, then
-//                   fp64 MSE, bias = sqrt(e[R]), optional copies.
+//  4. audit_sqerr   e_r = per-slice partial sums reduced in fixed order, one
+//                   thread per (prompt, replicate); fp64 partial sums of e_r
+//     audit_final   per prompt: MSE = fp64 mean of e_r, bias = sqrt(e[R]).
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -48,7 +48,7 @@ typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kCoefThreads = 64;     // replicates per audit_coeffs workgroup
-constexpr int kScanBytes = 64 << 10; // score bytes scanned per audit_coeffs workgroup (at most)
+constexpr int kSqThreads = 256;      // replicates per audit_sqerr workgroup
 constexpr int kMfmaThreads = 512;    // 8 waves per workgroup
 constexpr int kMfmaWaves = kMfmaThreads / kWave;
 constexpr int kTile = 32;            // replicate rows (and score columns) per matrix instruction
@@ -68,8 +68,8 @@ struct AuditLayout {
   int64_t rrows;     // ntiles * 32
   int64_t nslices;   // score-column slices per prompt
   int64_t nwg;       // audit_coeffs workgroups per prompt
-  int64_t slice;     // score columns scanned per audit_coeffs workgroup
-  size_t delta_off, epart_off, dsum_off, rmax_off, rexp_off, total;
+  int64_t nsq;       // audit_sqerr workgroups per prompt
+  size_t delta_off, epart_off, dsum_off, rpart_off, ebar_off, total;
 };
 
 AuditLayout audit_layout(int64_t B, int32_t gmax, int64_t D, int64_t R) {
@@ -79,10 +79,8 @@ AuditLayout audit_layout(int64_t B, int32_t gmax, int64_t D, int64_t R) {
   L.ntiles = (R + 1 + kTile - 1) / kTile;
   L.rrows = L.ntiles * kTile;
   L.nslices = (D + slice_cols(L.ks) - 1) / slice_cols(L.ks);
-  const int64_t by_reps = (R + kCoefThreads - 1) / kCoefThreads;
-  const int64_t by_scan = ((int64_t)gmax * D * 2 + kScanBytes - 1) / kScanBytes;
-  L.nwg = by_reps > by_scan ? by_reps : by_scan;
-  L.slice = round_up((D + L.nwg - 1) / L.nwg, 8);
+  L.nwg = (R + kCoefThreads - 1) / kCoefThreads;
+  L.nsq = (R + 1 + kSqThreads - 1) / kSqThreads;
   size_t off = 0;
   L.delta_off = off;
   off += (size_t)round_up(B * L.rrows * L.kp * 4, 256);            // fp32 delta rows
@@ -90,23 +88,22 @@ AuditLayout audit_layout(int64_t B, int32_t gmax, int64_t D, int64_t R) {
   off += (size_t)round_up(B * L.nslices * L.rrows * 4, 256);       // per-slice squared errors
   L.dsum_off = off;
   off += (size_t)round_up(B * L.nwg * gmax * 4, 256);               // partial delta sums
-  L.rmax_off = off;
-  off += (size_t)round_up(B * L.nwg * L.kp * 4, 256);               // partial row maxima
-  L.rexp_off = off;
-  off += (size_t)round_up(B * L.kp * 4, 256);                       // row exponents
+  L.rpart_off = off;
+  off += (size_t)round_up(B * L.nsq * 8, 256);                      // fp64 partial sums of e_r
+  L.ebar_off = off;
+  off += (size_t)round_up(B * 4, 256);                              // e of the delta_bar row
   L.total = off;
   return L;
 }
 
 // ---------------------------------------------------------------------------
-// 1. Replicate coefficients (+ row-magnitude scan).
+// 1. Replicate coefficients.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
     int64_t B, int64_t nv, int32_t gmax, int kp, const int64_t* __restrict__ offsets,
     const float* __restrict__ rewards, const float* __restrict__ p,
     const float* __restrict__ pi_w, uint64_t seed, int64_t rep0, int64_t R, int64_t nwg,
-    int64_t rrows, const uint16_t* __restrict__ scores, int64_t ld, int64_t D, int64_t slice,
-    float* __restrict__ delta, float* __restrict__ dsum, uint32_t* __restrict__ rmax,
+    int64_t rrows, float* __restrict__ delta, float* __restrict__ dsum,
     int32_t* __restrict__ edge_count, int32_t* d_status) {
   extern __shared__ float lds[];
   const int64_t b = blockIdx.x / nwg;
@@ -121,7 +118,6 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
   float* pl = A + kCoefThreads * stride;  // [gmax]            continuation probabilities
   float* af = pl + gmax;                  // [gmax]            complete-pair coefficients
   float* rl = af + gmax;                  // [gmax]            rewards
-  uint32_t* mx = reinterpret_cast<uint32_t*>(rl + gmax);  // [gmax] row magnitude maxima
 
   const bool vert = lane < g;
   const float r_i = vert ? rewards[o0 + lane] : 0.0f;
@@ -129,7 +125,6 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
   if (vert) {
     pl[lane] = p_i;
     rl[lane] = r_i;
-    mx[lane] = 0u;
     if (!p_in_range(p_i) && chunk == 0) raise_status(d_status, PAIR_ST_P_RANGE);
   }
 
@@ -169,44 +164,7 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
   }
   if (bad_rho && chunk == 0) raise_status(d_status, PAIR_ST_RHO_RANGE);
 
-  // Largest |s| of every row over this workgroup's column slice, as bf16
-  // magnitude bits (integer order = magnitude order for finite values).
-  {
-    const int64_t c_lo = chunk * slice;
-    const int64_t c_hi = c_lo + slice < D ? c_lo + slice : D;
-    const int64_t pieces_per_row = c_lo < c_hi ? (c_hi - c_lo + 7) / 8 : 0;
-    const int64_t pieces = g * pieces_per_row;
-    int cur = -1;
-    uint32_t m = 0;
-    for (int64_t q = lane; q < pieces; q += kWave) {
-      const int i = (int)(q / pieces_per_row);
-      const int64_t col = c_lo + 8 * (q - (int64_t)i * pieces_per_row);
-      const uint16_t* src = scores + (o0 + i) * ld + col;
-      if (i != cur) {
-        if (cur >= 0) atomicMax(&mx[cur], m);
-        cur = i;
-        m = 0;
-      }
-      if (col + 8 <= c_hi) {
-        const uint4 v = load_nt16(src);
-        const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const uint32_t lo = w4[k] & 0x7fffu, hi = (w4[k] >> 16) & 0x7fffu;
-          m = lo > m ? lo : m;
-          m = hi > m ? hi : m;
-        }
-      } else {
-        for (int64_t c = col; c < c_hi; ++c) {
-          const uint32_t h = src[c - col] & 0x7fffu;
-          m = h > m ? h : m;
-        }
-      }
-    }
-    if (cur >= 0) atomicMax(&mx[cur], m);
-  }
   __syncthreads();
-  if (vert) rmax[(b * nwg + chunk) * kp + lane] = mx[lane];
 
   // One replicate per lane.
   const int64_t rloc = chunk * kCoefThreads + lane;
@@ -278,40 +236,25 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// 2. delta_bar row, zero padding, per-row exponents.
+// 2. delta_bar row and zero padding.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void audit_prep_kernel(int64_t B, int64_t nv, int32_t gmax, int kp,
                                                          const int64_t* __restrict__ offsets,
                                                          int64_t R, int64_t nwg, int64_t rrows,
                                                          const float* __restrict__ dsum,
-                                                         const uint32_t* __restrict__ rmax,
-                                                         float* __restrict__ delta,
-                                                         int32_t* __restrict__ rexp,
-                                                         int32_t* d_status) {
+                                                         float* __restrict__ delta) {
   const int64_t b = blockIdx.x;
   int64_t o0, g;
   if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, nullptr, false)) return;
   const int tid = threadIdx.x;
   if (tid < kp) {
     float v = 0.0f;
-    int32_t ex = 0;
     if (tid < g) {
       float s = 0.0f;
-      uint32_t m = 0;
-      for (int64_t c = 0; c < nwg; ++c) {
-        s += dsum[(b * nwg + c) * gmax + tid];
-        const uint32_t mc = rmax[(b * nwg + c) * kp + tid];
-        m = mc > m ? mc : m;
-      }
+      for (int64_t c = 0; c < nwg; ++c) s += dsum[(b * nwg + c) * gmax + tid];
       v = s / (float)R;
-      if (m >= 0x7f80u) {                 // inf or NaN in the row
-        raise_status(d_status, PAIR_ST_NONFINITE);
-      } else if (m != 0u) {
-        ex = (int32_t)(m >> 7) - 127;     // 2^ex <= max |s| < 2^(ex+1); -127 for subnormals
-      }
     }
     delta[(b * rrows + R) * kp + tid] = v;
-    rexp[b * kp + tid] = ex;
   }
   const int64_t pad = (rrows - R - 1) * kp;
   float* dst = delta + (b * rrows + R + 1) * kp;
@@ -339,14 +282,18 @@ template <int KS>
 __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS == 1 ? 4 : 2))) void audit_mfma_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets, int64_t D,
     const uint16_t* __restrict__ scores, int64_t ld, int64_t rrows, int64_t ntiles,
-    int64_t nslices, const float* __restrict__ delta, const int32_t* __restrict__ rexp,
-    float* __restrict__ epart) {
+    int64_t nslices, const float* __restrict__ delta, float* __restrict__ epart,
+    int32_t* d_status) {
   constexpr int KP = 16 * KS;
   constexpr int SW = slice_cols(KS);
   constexpr int kSteps = SW / kTile;
   constexpr int kRowsLds = SW + SW / 8;
+  constexpr int kPieces = KP * (SW / 8);    // 16-byte pieces of the slice
+  constexpr int kPerThread = (kPieces + kMfmaThreads - 1) / kMfmaThreads;
   __shared__ __align__(16) uint16_t S_lds[kRowsLds * KP];
   __shared__ float tail_part[kMfmaWaves][kTile];
+  __shared__ uint32_t row_max[KP];
+  __shared__ int32_t ex[KP];
 
   // XCD-aware placement: hardware round-robins workgroup ids over 8 XCDs;
   // give each XCD a contiguous range of logical (prompt, slice) ids so the
@@ -362,36 +309,82 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
   const int lane = tid & (kWave - 1);
-  const int32_t* ex = rexp + b * KP;
   const int64_t col0 = sl * (int64_t)SW;
+  if (tid < KP) row_max[tid] = 0u;
+  __syncthreads();
 
-  // Stage the slice: 16-byte piece p -> row i = p % KP, columns d0 .. d0 + 7
-  // (d0 = 8 (p / KP)); values rescaled by 2^-e_i and converted to fp16
-  // (exact for every value within 2^17 of the row maximum), columns past D
-  // zero-filled.
+  // Stage the slice in two passes.  Pass 1 loads the 16-byte pieces
+  // (piece p -> row i = p % KP, columns d0 .. d0 + 7 with d0 = 8 (p / KP);
+  // columns past D and rows past G read as zero) and finds each row's largest
+  // magnitude within the slice as bf16 bits (integer order = magnitude
+  // order).  Pass 2 rescales row i by 2^-e_i, 2^e_i <= max |s_i| < 2^(e_i+1),
+  // and converts to fp16 (exact for every value within 2^17 of that
+  // maximum).
+  uint4 pv[kPerThread];
   {
     const uint16_t* sb = scores + o0 * ld;
-    for (int pidx = tid; pidx < KP * (SW / 8); pidx += kMfmaThreads) {
+    int cur = -1;
+    uint32_t m = 0;
+#pragma unroll
+    for (int t = 0; t < kPerThread; ++t) {
+      const int pidx = tid + t * kMfmaThreads;
+      uint4 v = make_uint4(0u, 0u, 0u, 0u);
+      if (pidx < kPieces) {
+        const int i = pidx % KP;
+        const int64_t col = col0 + 8 * (pidx / KP);
+        if (i < g) {
+          const uint16_t* src = sb + (int64_t)i * ld + col;
+          if (col + 8 <= D) {
+            v = load_nt16(src);
+          } else if (col < D) {
+            uint16_t h[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) h[e] = (col + e < D) ? src[e] : (uint16_t)0;
+            v.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+            v.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+            v.z = (uint32_t)h[4] | ((uint32_t)h[5] << 16);
+            v.w = (uint32_t)h[6] | ((uint32_t)h[7] << 16);
+          }
+        }
+        const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+        uint32_t mp = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t lo = w4[k] & 0x7fffu, hi = (w4[k] >> 16) & 0x7fffu;
+          mp = lo > mp ? lo : mp;
+          mp = hi > mp ? hi : mp;
+        }
+        if (i != cur) {
+          if (cur >= 0 && m != 0u) atomicMax(&row_max[cur], m);
+          cur = i;
+          m = 0;
+        }
+        m = mp > m ? mp : m;
+      }
+      pv[t] = v;
+    }
+    if (cur >= 0 && m != 0u) atomicMax(&row_max[cur], m);
+  }
+  __syncthreads();
+  if (tid < KP) {
+    const uint32_t mm = row_max[tid];
+    int32_t e = 0;
+    if (mm >= 0x7f80u) {                 // inf or NaN in the row
+      raise_status(d_status, PAIR_ST_NONFINITE);
+    } else if (mm != 0u) {
+      e = (int32_t)(mm >> 7) - 127;      // -127 for a row of subnormals
+    }
+    ex[tid] = e;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int t = 0; t < kPerThread; ++t) {
+    const int pidx = tid + t * kMfmaThreads;
+    if (pidx < kPieces) {
       const int i = pidx % KP;
       const int d0 = 8 * (pidx / KP);
-      const int64_t col = col0 + d0;
-      uint4 v = make_uint4(0u, 0u, 0u, 0u);
-      if (i < g) {
-        const uint16_t* src = sb + (int64_t)i * ld + col;
-        if (col + 8 <= D) {
-          v = load_nt16(src);
-        } else if (col < D) {
-          uint16_t h[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) h[e] = (col + e < D) ? src[e] : (uint16_t)0;
-          v.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
-          v.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
-          v.z = (uint32_t)h[4] | ((uint32_t)h[5] << 16);
-          v.w = (uint32_t)h[6] | ((uint32_t)h[7] << 16);
-        }
-      }
       const int ne = -ex[i];
-      const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+      const uint32_t w4[4] = {pv[t].x, pv[t].y, pv[t].z, pv[t].w};
       uint16_t* dst = &S_lds[(d0 + d0 / 8) * KP + i];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
@@ -535,37 +528,61 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
 }
 
 // ---------------------------------------------------------------------------
-// 4. Fixed-order reductions: e_r = sum over slices (fp32, slice order), then
-//    MSE = mean_r e_r (fp64) and bias = sqrt(e_R).
+// 4. Fixed-order reductions.  audit_sqerr: one thread per (prompt, replicate
+//    row) sums the per-slice partials in slice order (fp32) into e_r, and
+//    each workgroup writes the fp64 sum of its e_r; audit_final: per prompt,
+//    MSE = (sum of those partials in order) / R and bias = sqrt(e_R).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void audit_finalize_kernel(
+__global__ __launch_bounds__(kSqThreads) void audit_sqerr_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets, int64_t R,
-    int64_t rrows, int64_t nslices, const float* __restrict__ epart, double* __restrict__ mse,
-    double* __restrict__ bias_norm, float* __restrict__ rep_sqerr) {
-  __shared__ double part[256];
-  const int64_t b = blockIdx.x;
+    int64_t rrows, int64_t nslices, int64_t nsq, const float* __restrict__ epart,
+    double* __restrict__ rpart, float* __restrict__ ebar, float* __restrict__ rep_sqerr) {
+  __shared__ double part[kSqThreads / kWave];
+  const int64_t b = blockIdx.x / nsq;
+  const int64_t c = blockIdx.x - b * nsq;
   int64_t o0, g;
   if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, nullptr, false)) return;
-  const float* eb = epart + b * nslices * rrows;
-  double s = 0.0;
-  for (int64_t r = threadIdx.x; r < R; r += blockDim.x) {
-    float e = 0.0f;
-    for (int64_t k = 0; k < nslices; ++k) e += eb[k * rrows + r];
-    s += (double)e;
-    if (rep_sqerr != nullptr) rep_sqerr[b * R + r] = e;
+  const int64_t r = c * kSqThreads + threadIdx.x;
+  float e = 0.0f;
+  if (r <= R) {
+    const float* eb = epart + b * nslices * rrows + r;
+    int64_t k = 0;
+    for (; k + 8 <= nslices; k += 8) {
+      float v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = eb[(k + q) * rrows];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) e += v[q];
+    }
+    for (; k < nslices; ++k) e += eb[k * rrows];
+    if (r < R && rep_sqerr != nullptr) rep_sqerr[b * R + r] = e;
+    if (r == R) ebar[b] = e;
   }
-  part[threadIdx.x] = s;
+  double s = r < R ? (double)e : 0.0;
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) s += __shfl_xor(s, m, kWave);
+  const int wave = threadIdx.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == 0) part[wave] = s;
   __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
-    __syncthreads();
-  }
   if (threadIdx.x == 0) {
-    float eR = 0.0f;
-    for (int64_t k = 0; k < nslices; ++k) eR += eb[k * rrows + R];
-    mse[b] = part[0] / (double)R;
-    bias_norm[b] = sqrt((double)eR);
+    double t = 0.0;
+    for (int w = 0; w < kSqThreads / kWave; ++w) t += part[w];
+    rpart[b * nsq + c] = t;
   }
+}
+
+__global__ __launch_bounds__(256) void audit_final_kernel(
+    int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets, int64_t R,
+    int64_t nsq, const double* __restrict__ rpart, const float* __restrict__ ebar,
+    double* __restrict__ mse, double* __restrict__ bias_norm) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  int64_t o0, g;
+  if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, nullptr, false)) return;
+  double t = 0.0;
+  for (int64_t c = 0; c < nsq; ++c) t += rpart[b * nsq + c];
+  mse[b] = t / (double)R;
+  bias_norm[b] = sqrt((double)ebar[b]);
 }
 
 }  // namespace
@@ -584,29 +601,29 @@ int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, in
   float* delta = reinterpret_cast<float*>(ws + L.delta_off);
   float* epart = reinterpret_cast<float*>(ws + L.epart_off);
   float* dsum = reinterpret_cast<float*>(ws + L.dsum_off);
-  uint32_t* rmax = reinterpret_cast<uint32_t*>(ws + L.rmax_off);
-  int32_t* rexp = reinterpret_cast<int32_t*>(ws + L.rexp_off);
+  double* rpart = reinterpret_cast<double*>(ws + L.rpart_off);
+  float* ebar = reinterpret_cast<float*>(ws + L.ebar_off);
   const uint16_t* s = static_cast<const uint16_t*>(scores);
 
   const int64_t coef_grid = B * L.nwg;
   if (coef_grid > 0x7fffffffLL) return PAIR_ERANGE;
   const size_t coef_lds = ((size_t)gmax * (gmax + 1) + (size_t)kCoefThreads * (gmax + 1) +
-                           4 * (size_t)gmax) * sizeof(float);
+                           3 * (size_t)gmax) * sizeof(float);
   hipLaunchKernelGGL(audit_coeffs_kernel, dim3((unsigned)coef_grid), dim3(kCoefThreads), coef_lds,
                      stream, B, nv, gmax, L.kp, offsets, rewards, p, pi_w, seed, rep0, R, L.nwg,
-                     L.rrows, s, ld, D, L.slice, delta, dsum, rmax, edge_count, d_status);
+                     L.rrows, delta, dsum, edge_count, d_status);
   if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
 
   hipLaunchKernelGGL(audit_prep_kernel, dim3((unsigned)B), dim3(256), 0, stream, B, nv, gmax, L.kp,
-                     offsets, R, L.nwg, L.rrows, dsum, rmax, delta, rexp, d_status);
+                     offsets, R, L.nwg, L.rrows, dsum, delta);
   if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
 
   const int64_t grid = round_up(B * L.nslices, 8);
   if (grid > 0x7fffffffLL) return PAIR_ERANGE;
 #define PAIR_AUDIT_MFMA(KS_)                                                                   \
   hipLaunchKernelGGL(audit_mfma_kernel<KS_>, dim3((unsigned)grid), dim3(kMfmaThreads), 0, stream, \
-                     B, nv, gmax, offsets, D, s, ld, L.rrows, L.ntiles, L.nslices, delta, rexp,  \
-                     epart)
+                     B, nv, gmax, offsets, D, s, ld, L.rrows, L.ntiles, L.nslices, delta, epart, \
+                     d_status)
   switch (L.ks) {
     case 1: PAIR_AUDIT_MFMA(1); break;
     case 2: PAIR_AUDIT_MFMA(2); break;
@@ -616,8 +633,14 @@ int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, in
 #undef PAIR_AUDIT_MFMA
   if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
 
-  hipLaunchKernelGGL(audit_finalize_kernel, dim3((unsigned)B), dim3(256), 0, stream, B, nv, gmax,
-                     offsets, R, L.rrows, L.nslices, epart, mse, bias_norm, rep_sqerr);
+  const int64_t sq_grid = B * L.nsq;
+  if (sq_grid > 0x7fffffffLL) return PAIR_ERANGE;
+  hipLaunchKernelGGL(audit_sqerr_kernel, dim3((unsigned)sq_grid), dim3(kSqThreads), 0, stream, B,
+                     nv, gmax, offsets, R, L.rrows, L.nslices, L.nsq, epart, rpart, ebar,
+                     rep_sqerr);
+  if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
+  hipLaunchKernelGGL(audit_final_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, stream,
+                     B, nv, gmax, offsets, R, L.nsq, rpart, ebar, mse, bias_norm);
   return hipGetLastError() == hipSuccess ? PAIR_OK : PAIR_EHIP;
 }
 
