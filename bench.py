@@ -18,6 +18,8 @@ weighted-gradient kernel (the kernel `value` measures), timed with HIP events
 on the stream it is launched on.
 
 Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--no-cpu-baseline]
+       python bench.py --copy-calibration     (1 GiB copy for counter scaling)
+       python bench.py --record-traffic DIR   (counter runs -> profiles/counters.json)
 """
 from __future__ import annotations
 
@@ -62,6 +64,86 @@ def _traffic(kernel, sources):
     if not rec or rec.get("source_sha") != _source_sha(*sources):
         return None
     return rec.get("hbm_bytes_per_launch")
+
+
+# Kernels whose HBM traffic is recorded from rocprofv3 counter runs of this
+# script: key -> (kernel-name prefix of every dispatch the entry point makes,
+# name of the dispatch counted once per call, sources the record is tied to).
+TRAFFIC_KERNELS = {
+    "wgrad_b128": ("wgrad_kernel", "wgrad_kernel", ["wgrad.hip", "common.hpp"]),
+    "audit_b256": ("audit_", "audit_final_kernel", ["audit.hip", "common.hpp"]),
+}
+
+
+def _counter_rows(path):
+    import csv
+    with open(path, newline="") as f:
+        return [(r["Kernel_Name"], float(r["Counter_Value"])) for r in csv.DictReader(f)]
+
+
+def _kernel_kib(rows, prefix, per_call):
+    """KiB per entry-point call: all dispatches whose demangled name starts
+    with `prefix` (namespaces dropped), over the number of `per_call` ones."""
+    def base(name):
+        name = name.replace("(anonymous namespace)::", "")
+        name = name[5:] if name.startswith("void ") else name
+        return name.split("(")[0].split("<")[0].split("::")[-1].strip()
+    tot = sum(v for n, v in rows if base(n).startswith(prefix))
+    calls = sum(1 for n, _ in rows if base(n) == per_call)
+    if calls == 0:
+        raise SystemExit(f"no {per_call} dispatch in the counter file")
+    return tot / calls
+
+
+def record_traffic(folder):
+    """Write HBM bytes per launch into the committed counter record from four
+    rocprofv3 --pmc runs under `folder`: tr_FETCH_SIZE/, tr_WRITE_SIZE/ (this
+    script with --no-cpu-baseline --steps 2 --warmup 1) and trc_FETCH_SIZE/,
+    trc_WRITE_SIZE/ (this script with --copy-calibration).  Each counter is
+    scaled by the factor that maps it to the known bytes of the calibration
+    copy (1 GiB read, 1 GiB written)."""
+    def rows(sub):
+        return _counter_rows(os.path.join(folder, sub, "run_counter_collection.csv"))
+
+    gib = float(1 << 30)
+    factors = {}
+    for ctr in ("FETCH_SIZE", "WRITE_SIZE"):
+        copies = [v for n, v in rows("trc_" + ctr) if "copyBuffer" in n]
+        big = sorted(v for v in copies if v > 0.5 * max(copies))
+        factors[ctr] = (gib, big[len(big) // 2])
+    fetch_f = factors["FETCH_SIZE"][0] / (factors["FETCH_SIZE"][1] * 1024.0)
+    write_f = factors["WRITE_SIZE"][0] / (factors["WRITE_SIZE"][1] * 1024.0)
+    try:
+        with open(COUNTERS) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        rec = {}
+    fetch_rows, write_rows = rows("tr_FETCH_SIZE"), rows("tr_WRITE_SIZE")
+    cmd = "rocprofv3 --pmc {c} -f csv -d <out> -o run -- python -u <repo>/bench.py {a}"
+    for key, (prefix, per_call, sources) in TRAFFIC_KERNELS.items():
+        fk = _kernel_kib(fetch_rows, prefix, per_call)
+        wk = _kernel_kib(write_rows, prefix, per_call)
+        rd, wr = fk * 1024.0 * fetch_f, wk * 1024.0 * write_f
+        rec[key] = {
+            "kernels": prefix + "*",
+            "source_sha": _source_sha(*sources),
+            "fetch_size_kib_per_launch": round(fk, 1),
+            "write_size_kib_per_launch": round(wk, 1),
+            "calibration": {
+                "fetch_factor": round(fetch_f, 4), "write_factor": round(write_f, 4),
+                "basis": "plain 1 GiB device copy: FETCH_SIZE %.0f KiB, WRITE_SIZE %.0f KiB"
+                         % (factors["FETCH_SIZE"][1], factors["WRITE_SIZE"][1])},
+            "hbm_read_bytes_per_launch": int(rd),
+            "hbm_write_bytes_per_launch": int(wr),
+            "hbm_bytes_per_launch": int(rd + wr),
+            "commands": [cmd.format(c=c, a=a) for a in
+                         ("--no-cpu-baseline --steps 2 --warmup 1", "--copy-calibration")
+                         for c in ("FETCH_SIZE", "WRITE_SIZE")],
+        }
+    with open(COUNTERS, "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    print(json.dumps({k: rec[k]["hbm_bytes_per_launch"] for k in TRAFFIC_KERNELS}))
 
 
 def cpu_baseline(meta, w, scores_dev, meta_a, wa, scores_a_dev, budget_s=12.0):
@@ -116,16 +198,33 @@ def cpu_baseline(meta, w, scores_dev, meta_a, wa, scores_a_dev, budget_s=12.0):
 
 
 def copy_calibration(gib=1.0, reps=5):
-    """Plain device copy of known size, for scaling rocprofv3 FETCH/WRITE counters."""
+    """Plain device copy of known size, for scaling rocprofv3 FETCH/WRITE
+    counters, timed with events; also a read-only reduction over a 4x larger
+    buffer as a measured read ceiling."""
     import torch
 
     n = int(gib * (1 << 30)) // 2
     src = torch.empty(n, dtype=torch.bfloat16, device="cuda:0").normal_()
     dst = torch.empty_like(src)
+    big = torch.empty(4 * n, dtype=torch.bfloat16, device="cuda:0").normal_()
+    for _ in range(2):
+        dst.copy_(src)
+        big.sum()
+    torch.cuda.synchronize()
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    e[0].record()
     for _ in range(reps):
         dst.copy_(src)
+    e[1].record()
+    for _ in range(reps):
+        big.sum()
+    e[2].record()
     torch.cuda.synchronize()
-    print(json.dumps({"copy_calibration_bytes": n * 2, "reps": reps}), flush=True)
+    copy_ms = e[0].elapsed_time(e[1]) / reps
+    read_ms = e[1].elapsed_time(e[2]) / reps
+    print(json.dumps({"copy_calibration_bytes": n * 2, "reps": reps,
+                      "copy_GBps": round(2 * n * 2 / (copy_ms * 1e-3) / 1e9, 1),
+                      "read_GBps": round(4 * n * 2 / (read_ms * 1e-3) / 1e9, 1)}), flush=True)
 
 
 def main():
@@ -135,7 +234,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--record-traffic", metavar="DIR",
+                    help="write profiles/counters.json from rocprofv3 --pmc runs under DIR")
     args = ap.parse_args()
+
+    if args.record_traffic:
+        record_traffic(args.record_traffic)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one MI355X: this build runs on a single GPU "
@@ -196,7 +301,7 @@ def main():
         ev[1].record(stream)
         pair.pair_edge_coeffs(B, nv, G, off, rew, mask[0], pi, coeff, None, status, stream)
         ev[2].record(stream)
-        pair.pair_weighted_grad(B, nv, off, scores, coeff, out, status, stream)
+        pair.pair_weighted_grad(B, nv, off, scores, coeff, out, 0, status, stream)
         ev[3].record(stream)
         pair.pair_audit(Ba, nva, Ga, off_a, scores_a, rew_a, p_a, None, wa.design_seed, 0, R, mse,
                         bias, reps, ec_a, ws, status, stream)
