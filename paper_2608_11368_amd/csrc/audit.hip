@@ -10,12 +10,12 @@
 // ||delta_bar S_b|| for the bias (delta_bar = mean_r delta_r).
 //
 // Pipeline (all on the caller's stream):
-//  1. audit_coeffs  one wave per (prompt, 64 replicates), one lane per
+//  1. audit_coeffs  one workgroup per (prompt, 256 replicates), one lane per
 //                   replicate: Philox draw of J^(r) (same counter reading as
 //                   the design draw), the coefficient fold over a per-prompt
 //                   table W_ij = (r_i - r_j)/rho_ij in LDS, centring over the
 //                   completed vertices, delta_r stored in fp32, and a
-//                   fixed-order partial sum of delta over the 64 lanes.
+//                   fixed-order partial sum of delta over the 256 lanes.
 //  2. audit_prep    delta_bar appended as replicate row R, padding rows
 //                   zeroed.
 //  3. audit_mfma    the contraction on v_mfma_f32_32x32x16_f16.  Each score
@@ -47,7 +47,7 @@ namespace {
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kCoefThreads = 64;     // replicates per audit_coeffs workgroup
+constexpr int kCoefThreads = 256;    // replicates per audit_coeffs workgroup
 constexpr int kSqThreads = 256;      // replicates per audit_sqerr workgroup
 constexpr int kMfmaThreads = 512;    // 8 waves per workgroup
 constexpr int kMfmaWaves = kMfmaThreads / kWave;
@@ -97,56 +97,60 @@ AuditLayout audit_layout(int64_t B, int32_t gmax, int64_t D, int64_t R) {
 }
 
 // ---------------------------------------------------------------------------
-// 1. Replicate coefficients.
+// 1. Replicate coefficients.  A workgroup owns one prompt and 256 replicates
+//    (one per lane).  The edge table W, the probabilities and the
+//    complete-pair coefficients are built once per workgroup in LDS; each lane
+//    then draws its indicators, folds c_i = sum_j J_j W_ij with W read by
+//    broadcast (W_ii = 0, so no j != i test is needed, and a zero indicator
+//    adds exactly nothing), centres, and keeps its KP deviations in registers.
 // ---------------------------------------------------------------------------
+template <int KP>
 __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
-    int64_t B, int64_t nv, int32_t gmax, int kp, const int64_t* __restrict__ offsets,
+    int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets,
     const float* __restrict__ rewards, const float* __restrict__ p,
     const float* __restrict__ pi_w, uint64_t seed, int64_t rep0, int64_t R, int64_t nwg,
     int64_t rrows, float* __restrict__ delta, float* __restrict__ dsum,
     int32_t* __restrict__ edge_count, int32_t* d_status) {
-  extern __shared__ float lds[];
+  constexpr int kWaves = kCoefThreads / kWave;
+  __shared__ __align__(16) float W[KP * KP];     // (r_i - r_j) / rho_ij, zero on and past G
+  __shared__ float pl[KP], rl[KP], af[KP];
+  __shared__ float wsum[kWaves][KP];
   const int64_t b = blockIdx.x / nwg;
   const int64_t chunk = blockIdx.x - b * nwg;
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
   int64_t o0, g;
-  if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, d_status, chunk == 0 && lane == 0)) return;
+  if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, d_status, chunk == 0 && tid == 0)) return;
 
-  const int stride = gmax + 1;
-  float* W = lds;                         // [gmax][gmax + 1]  (r_i - r_j) / rho_ij
-  float* A = W + gmax * stride;           // [64][gmax + 1]    per-replicate values
-  float* pl = A + kCoefThreads * stride;  // [gmax]            continuation probabilities
-  float* af = pl + gmax;                  // [gmax]            complete-pair coefficients
-  float* rl = af + gmax;                  // [gmax]            rewards
-
-  const bool vert = lane < g;
-  const float r_i = vert ? rewards[o0 + lane] : 0.0f;
-  const float p_i = vert ? p[o0 + lane] : 1.0f;
-  if (vert) {
-    pl[lane] = p_i;
-    rl[lane] = r_i;
-    if (!p_in_range(p_i) && chunk == 0) raise_status(d_status, PAIR_ST_P_RANGE);
+  if (wave == 0) {
+    const bool vert = lane < g;
+    const float r_i = vert ? rewards[o0 + lane] : 0.0f;
+    const float p_i = vert ? p[o0 + lane] : 1.0f;
+    if (lane < KP) {
+      pl[lane] = p_i;
+      rl[lane] = r_i;
+    }
+    if (vert && !p_in_range(p_i) && chunk == 0) raise_status(d_status, PAIR_ST_P_RANGE);
+    // Complete-pair coefficients: the same fold with every vertex completed
+    // and rho = 1, centred over all G vertices.
+    float cf = 0.0f;
+    for (int j = 0; j < g; ++j) {
+      const float r_j = __shfl(r_i, j, kWave);
+      if (vert && j != lane) cf += r_i - r_j;
+    }
+    float a_full = vert ? cf / (float)(g * (g - 1)) : 0.0f;
+    const float tot = wave_sum(a_full);
+    a_full = vert ? a_full - tot / (float)g : 0.0f;
+    if (lane < KP) af[lane] = a_full;
   }
-
-  // Complete-pair coefficients: the same fold with every vertex completed
-  // and rho = 1, centred over all G vertices.
-  float cf = 0.0f;
-  for (int j = 0; j < g; ++j) {
-    const float r_j = __shfl(r_i, j, kWave);
-    if (vert && j != lane) cf += r_i - r_j;
-  }
-  float a_full = vert ? cf / (float)(g * (g - 1)) : 0.0f;
-  const float tot = wave_sum(a_full);
-  a_full = vert ? a_full - tot / (float)g : 0.0f;
-  if (vert) af[lane] = a_full;
   __syncthreads();
 
-  // Per-prompt edge table.
   bool bad_rho = false;
-  for (int64_t idx = lane; idx < g * g; idx += kWave) {
-    const int i = (int)(idx / g), j = (int)(idx - (int64_t)i * g);
+  for (int idx = tid; idx < KP * KP; idx += kCoefThreads) {
+    const int i = idx / KP, j = idx - i * KP;
     float w = 0.0f;
-    if (i != j) {
+    if (i != j && i < g && j < g) {
       float rho;
       if (pi_w != nullptr) {
         const int lo = i < j ? i : j, hi = i < j ? j : i;
@@ -160,14 +164,13 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
         bad_rho = true;
       }
     }
-    W[i * stride + j] = w;
+    W[idx] = w;
   }
   if (bad_rho && chunk == 0) raise_status(d_status, PAIR_ST_RHO_RANGE);
-
   __syncthreads();
 
-  // One replicate per lane.
-  const int64_t rloc = chunk * kCoefThreads + lane;
+  // Indicators of this lane's replicate.
+  const int64_t rloc = chunk * kCoefThreads + tid;
   const bool valid = rloc < R;
   uint64_t bits = 0;
   if (valid) {
@@ -187,51 +190,53 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
   }
   const int k = __popcll(bits);
   if (valid && edge_count != nullptr) edge_count[b * R + rloc] = k * (k - 1) / 2;
+  if (k < 2) bits = 0;   // fewer than two completed vertices: A~ = 0
 
-  // Fold: A~_i = (1/(G(G-1))) sum_{j observed, j != i} W_ij, then centre.
+  // Fold: A~_i = J_i (1/(G(G-1))) sum_j J_j W_ij, in ascending j; then centre
+  // over the completed vertices.
+  float m[KP], d[KP];
+#pragma unroll
+  for (int j = 0; j < KP; ++j) m[j] = ((bits >> j) & 1ull) ? 1.0f : 0.0f;
   const float den = (float)(g * (g - 1));
   float sum_obs = 0.0f;
-  for (int i = 0; i < g; ++i) {
-    float ai = 0.0f;
-    if (k >= 2 && ((bits >> i) & 1ull)) {
-      float c = 0.0f;
-      for (int j = 0; j < g; ++j)
-        if (j != i && ((bits >> j) & 1ull)) c += W[i * stride + j];
-      ai = c / den;
-      sum_obs += ai;
+#pragma unroll
+  for (int i = 0; i < KP; ++i) {
+    float c = 0.0f;
+#pragma unroll
+    for (int j0 = 0; j0 < KP; j0 += 4) {
+      const float4 w4 = *reinterpret_cast<const float4*>(&W[i * KP + j0]);
+      c = __builtin_fmaf(m[j0], w4.x, c);
+      c = __builtin_fmaf(m[j0 + 1], w4.y, c);
+      c = __builtin_fmaf(m[j0 + 2], w4.z, c);
+      c = __builtin_fmaf(m[j0 + 3], w4.w, c);
     }
-    A[lane * stride + i] = ai;
+    const float ai = m[i] != 0.0f ? c / den : 0.0f;
+    sum_obs += ai;
+    d[i] = ai;
   }
   const float mean = k >= 2 ? sum_obs / (float)k : 0.0f;
-
-  // delta = A~ - a (fp32, zero padded to kp); kept in LDS for the column sums.
-  if (rloc < rrows) {
-    float* drow = delta + (b * rrows + rloc) * kp;
-    for (int i0 = 0; i0 < kp; i0 += 4) {
-      float v4[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int i = i0 + q;
-        float dv = 0.0f;
-        if (i < g) {
-          const float ai = (k >= 2 && ((bits >> i) & 1ull)) ? A[lane * stride + i] - mean : 0.0f;
-          dv = valid ? ai - af[i] : 0.0f;
-          A[lane * stride + i] = dv;
-        }
-        v4[q] = dv;
-      }
-      if (valid) *reinterpret_cast<float4*>(drow + i0) = make_float4(v4[0], v4[1], v4[2], v4[3]);
-    }
-  } else {
-    for (int i = 0; i < g; ++i) A[lane * stride + i] = 0.0f;
+  for (int i = 0; i < KP; ++i) d[i] = valid ? (m[i] != 0.0f ? d[i] - mean : 0.0f) - af[i] : 0.0f;
+
+  if (valid) {
+    float* drow = delta + (b * rrows + rloc) * KP;
+#pragma unroll
+    for (int i0 = 0; i0 < KP; i0 += 4)
+      *reinterpret_cast<float4*>(drow + i0) = make_float4(d[i0], d[i0 + 1], d[i0 + 2], d[i0 + 3]);
+  }
+
+  // Fixed-order column sums: butterfly within each wave, then waves in order.
+#pragma unroll
+  for (int i = 0; i < KP; ++i) {
+    const float sw = wave_sum(d[i]);
+    if (lane == 0) wsum[wave][i] = sw;
   }
   __syncthreads();
-
-  // Fixed-order column sums over this workgroup's replicates.
-  if (vert) {
-    float s = 0.0f;
-    for (int t = 0; t < kCoefThreads; ++t) s += A[t * stride + lane];
-    dsum[(b * nwg + chunk) * gmax + lane] = s;
+  if (tid < g) {
+    float sc = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) sc += wsum[w][tid];
+    dsum[(b * nwg + chunk) * gmax + tid] = sc;
   }
 }
 
@@ -607,11 +612,17 @@ int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, in
 
   const int64_t coef_grid = B * L.nwg;
   if (coef_grid > 0x7fffffffLL) return PAIR_ERANGE;
-  const size_t coef_lds = ((size_t)gmax * (gmax + 1) + (size_t)kCoefThreads * (gmax + 1) +
-                           3 * (size_t)gmax) * sizeof(float);
-  hipLaunchKernelGGL(audit_coeffs_kernel, dim3((unsigned)coef_grid), dim3(kCoefThreads), coef_lds,
-                     stream, B, nv, gmax, L.kp, offsets, rewards, p, pi_w, seed, rep0, R, L.nwg,
-                     L.rrows, delta, dsum, edge_count, d_status);
+#define PAIR_AUDIT_COEFFS(KP_)                                                                  \
+  hipLaunchKernelGGL(audit_coeffs_kernel<KP_>, dim3((unsigned)coef_grid), dim3(kCoefThreads), 0, \
+                     stream, B, nv, gmax, offsets, rewards, p, pi_w, seed, rep0, R, L.nwg,       \
+                     L.rrows, delta, dsum, edge_count, d_status)
+  switch (L.ks) {
+    case 1: PAIR_AUDIT_COEFFS(16); break;
+    case 2: PAIR_AUDIT_COEFFS(32); break;
+    case 3: PAIR_AUDIT_COEFFS(48); break;
+    default: PAIR_AUDIT_COEFFS(64); break;
+  }
+#undef PAIR_AUDIT_COEFFS
   if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
 
   hipLaunchKernelGGL(audit_prep_kernel, dim3((unsigned)B), dim3(256), 0, stream, B, nv, gmax, L.kp,
