@@ -18,6 +18,13 @@ Parity status of each function (what pins it, see ``tests/test_oracle_pins.py``)
   audit             pinned: exact design covariance trace (Prop 1) by
                     enumeration; Gram-matrix identity for every replicate;
                     bias^2 ~ MSE/R statistics; p == 1 gives zero MSE
+  *_rule variants   pinned by exhaustive design enumeration against the
+                    expectations the paper states for each edge-weight rule
+                    (naive bias, clipped multiplier min(1, w_max rho) - 1,
+                    ratio estimator exact under a self-weighting design),
+                    cross-rule identities, ESS special cases; the
+                    marginal-only rule against its own enumeration closed
+                    form (a reading: the paper names it without a formula)
 """
 from __future__ import annotations
 
@@ -33,6 +40,16 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 
 F32 = 0
 BF16 = 1
+
+# Edge-weight rules (same codes as the C oracle; see pair_oracle.c).
+RULE_HT = 0
+RULE_UNWEIGHTED = 1
+RULE_RATIO_KE = 2
+RULE_CLIPPED = 3
+RULE_SELFNORM = 4
+RULE_MARGINAL = 5
+RULES = {"ht": RULE_HT, "unweighted": RULE_UNWEIGHTED, "ratio_ke": RULE_RATIO_KE,
+         "clipped": RULE_CLIPPED, "selfnorm": RULE_SELFNORM, "marginal": RULE_MARGINAL}
 
 ERRORS = {
     0: "ok",
@@ -82,6 +99,15 @@ def _load():
         lib.orc_audit.argtypes = [i64, P, i32, i64, P, ctypes.c_int, i64, P, P, P, u64, i64, i64,
                                   P, P, P, P, P]
         lib.orc_audit.restype = ctypes.c_int
+        dbl = ctypes.c_double
+        lib.orc_pair_grad_rule.argtypes = [i64, P, i32, i64, P, ctypes.c_int, i64, P, P, P,
+                                           ctypes.c_int, dbl, P, P, P, P]
+        lib.orc_pair_grad_rule.restype = ctypes.c_int
+        lib.orc_pair_coeffs_rule.argtypes = [i64, P, i32, P, P, P, ctypes.c_int, dbl, P, P, P, P]
+        lib.orc_pair_coeffs_rule.restype = ctypes.c_int
+        lib.orc_audit_rule.argtypes = [i64, P, i32, i64, P, ctypes.c_int, i64, P, P, P,
+                                       ctypes.c_int, dbl, u64, i64, i64, P, P, P, P, P]
+        lib.orc_audit_rule.restype = ctypes.c_int
         lib.orc_num_threads.argtypes = []
         lib.orc_num_threads.restype = ctypes.c_int
         _lib = lib
@@ -149,6 +175,58 @@ def design_inclusion(offsets, p, seed, rep0, R, gmax, prompt_id=None, want_pi=Tr
     return {"mask": mask, "pi": pi, "edge_count": ec, "completed": comp}
 
 
+def _gmax(off, pi, gmax):
+    if pi is not None:
+        return pi.shape[-1]
+    if gmax is None:
+        return int(np.max(np.diff(off)))
+    return gmax
+
+
+def pair_grad_rule(offsets, scores, rewards, mask=None, pi=None, rule=RULE_HT, wmax=0.0,
+                   gmax=None):
+    """Per-prompt estimate under an edge-weight rule, by explicit edges in fp64.
+    Returns dict(out[B][D], edge_count[B], ess[B], max_weight[B])."""
+    lib = _load()
+    off = _offsets(offsets)
+    B = off.size - 1
+    s, code, ld = _scores_arg(scores)
+    D = s.shape[1]
+    r = np.ascontiguousarray(rewards, dtype=np.float32)
+    m = None if mask is None else np.ascontiguousarray(mask, dtype=np.uint8)
+    if pi is not None:
+        pi = np.ascontiguousarray(pi, dtype=np.float32)
+    gmax = _gmax(off, pi, gmax)
+    out = np.zeros((B, D), dtype=np.float64)
+    ec = np.zeros(B, dtype=np.int32)
+    ess = np.zeros(B, dtype=np.float64)
+    mw = np.zeros(B, dtype=np.float64)
+    _check(lib.orc_pair_grad_rule(B, _ptr(off), gmax, D, _ptr(s), code, ld, _ptr(r), _ptr(m),
+                                  _ptr(pi), int(rule), float(wmax), _ptr(out), _ptr(ec), _ptr(ess),
+                                  _ptr(mw)))
+    return {"out": out, "edge_count": ec, "ess": ess, "max_weight": mw}
+
+
+def pair_coeffs_rule(offsets, rewards, mask=None, pi=None, rule=RULE_HT, wmax=0.0, gmax=None):
+    """Sequence advantages under an edge-weight rule (Algorithm 1's edge order).
+    Returns dict(coeff[nv], edge_count[B], ess[B], max_weight[B])."""
+    lib = _load()
+    off = _offsets(offsets)
+    B = off.size - 1
+    r = np.ascontiguousarray(rewards, dtype=np.float32)
+    m = None if mask is None else np.ascontiguousarray(mask, dtype=np.uint8)
+    if pi is not None:
+        pi = np.ascontiguousarray(pi, dtype=np.float32)
+    gmax = _gmax(off, pi, gmax)
+    coeff = np.zeros(int(off[-1]), dtype=np.float64)
+    ec = np.zeros(B, dtype=np.int32)
+    ess = np.zeros(B, dtype=np.float64)
+    mw = np.zeros(B, dtype=np.float64)
+    _check(lib.orc_pair_coeffs_rule(B, _ptr(off), gmax, _ptr(r), _ptr(m), _ptr(pi), int(rule),
+                                    float(wmax), _ptr(coeff), _ptr(ec), _ptr(ess), _ptr(mw)))
+    return {"coeff": coeff, "edge_count": ec, "ess": ess, "max_weight": mw}
+
+
 def pair_grad(offsets, scores, rewards, mask=None, pi=None, gmax=None):
     """Eq. (pair-ht) per prompt in fp64: returns (out[B][D] float64, edge_count[B])."""
     lib = _load()
@@ -189,8 +267,9 @@ def pair_coeffs(offsets, rewards, mask=None, pi=None, gmax=None):
 
 
 def audit(offsets, scores, rewards, p, seed, rep0, R, pi_w=None, gmax=None, prompt_id=None,
-          want_reps=True):
-    """Frozen-population audit: returns dict(mse[B], bias_norm[B], rep_sqerr[B][R], edge_count[B][R])."""
+          want_reps=True, rule=RULE_HT, wmax=0.0):
+    """Frozen-population audit of the estimator under `rule`: returns
+    dict(mse[B], bias_norm[B], rep_sqerr[B][R], edge_count[B][R])."""
     lib = _load()
     off = _offsets(offsets)
     B = off.size - 1
@@ -208,6 +287,7 @@ def audit(offsets, scores, rewards, p, seed, rep0, R, pi_w=None, gmax=None, prom
     bias = np.zeros(B, dtype=np.float64)
     reps = np.zeros((B, R), dtype=np.float64) if want_reps else None
     ec = np.zeros((B, R), dtype=np.int32) if want_reps else None
-    _check(lib.orc_audit(B, _ptr(off), gmax, D, _ptr(s), code, ld, _ptr(r), _ptr(pp), _ptr(pi_w),
-                         seed, rep0, R, _ptr(pid), _ptr(mse), _ptr(bias), _ptr(reps), _ptr(ec)))
+    _check(lib.orc_audit_rule(B, _ptr(off), gmax, D, _ptr(s), code, ld, _ptr(r), _ptr(pp),
+                              _ptr(pi_w), int(rule), float(wmax), seed, rep0, R, _ptr(pid),
+                              _ptr(mse), _ptr(bias), _ptr(reps), _ptr(ec)))
     return {"mse": mse, "bias_norm": bias, "rep_sqerr": reps, "edge_count": ec}

@@ -24,7 +24,11 @@
  *   - App. B "At least two completed vertices": a draw with fewer than two
  *                                    completed vertices contributes zero
  *   - Sec. 5.2 frozen-policy audit and App. D metrics: MSE = E||g^ - g_full||^2,
- *                                    bias = || mean_r g^_r - g_full ||
+ *                                    bias = || mean_r g^_r - g_full ||,
+ *                                    ESS = (sum_e w_e)^2 / sum_e w_e^2
+ *   - App. A "Naive selection bias" and App. B "Estimated and stabilized
+ *     propensities": the estimator variants of Tables 4 and 5 (edge-weight
+ *     rules, below)
  *
  * Random design draws.  The paper only requires fresh randomisation for the
  * continuation indicators.  This oracle fixes one counter-based generator, the
@@ -51,6 +55,27 @@
 
 #define ORC_F32 0
 #define ORC_BF16 1
+
+/* Edge-weight rules.  Every rule estimates
+ *     g = (1/N) sum_{i<j observed} 1/2 (r_i - r_j) (w_i s_i - w_j s_j)
+ * with the weights (w_i, w_j) on the two halves of the edge term h_ij and the
+ * normaliser N:
+ *   HT          w_i = w_j = 1/rho_ij,              N = M = C(G, 2)   Eq. (pair-ht)
+ *   UNWEIGHTED  w_i = w_j = 1,                     N = M             (naive, g~_0)
+ *   RATIO_KE    w_i = w_j = 1,                     N = K_E           (observed-edge mean)
+ *   CLIPPED     w_i = w_j = min(1/rho_ij, w_max),  N = M
+ *   SELFNORM    w_i = w_j = 1/rho_ij,              N = sum_e I_e / rho_e   (Hajek)
+ *   MARGINAL    w_i = 1/pi_i, w_j = 1/pi_j,        N = M   (per-rollout propensity only;
+ *               pi_i is the diagonal of the logged block)
+ * A draw with no observed edge gives the zero vector under every rule.  The
+ * edge weight entering ESS and the maximum weight is w_i = w_j for the
+ * symmetric rules and (w_i + w_j) / 2 for MARGINAL. */
+#define ORC_RULE_HT 0
+#define ORC_RULE_UNWEIGHTED 1
+#define ORC_RULE_RATIO_KE 2
+#define ORC_RULE_CLIPPED 3
+#define ORC_RULE_SELFNORM 4
+#define ORC_RULE_MARGINAL 5
 
 /* ------------------------------------------------------------------------ */
 /* Philox4x64-10, written from the SC'11 description: each round multiplies  */
@@ -189,17 +214,48 @@ static double rho_of(const float* blk, int32_t gmax, int64_t i, int64_t j) {
     return (double)blk[lo * gmax + hi];
 }
 
+/* Weights of the two halves of observed edge (i, j) under `rule` (see the
+ * rule table above), and the edge's share 1/rho_ij of the self-normalised
+ * denominator.  blk == NULL means rho == pi == 1. */
+static int edge_weights(int rule, double wmax, const float* blk, int32_t gmax, int64_t i,
+                        int64_t j, double* wi, double* wj, double* inv_rho) {
+    double rho = blk ? rho_of(blk, gmax, i, j) : 1.0;
+    *inv_rho = 0.0;
+    if (rule == ORC_RULE_HT || rule == ORC_RULE_CLIPPED || rule == ORC_RULE_SELFNORM) {
+        if (!(rho > 0.0 && rho <= 1.0)) return ORC_ERHO;
+        double w = 1.0 / rho;
+        if (rule == ORC_RULE_CLIPPED && w > wmax) w = wmax;
+        *wi = *wj = w;
+        *inv_rho = 1.0 / rho;
+    } else if (rule == ORC_RULE_MARGINAL) {
+        double pii = blk ? (double)blk[i * gmax + i] : 1.0;
+        double pjj = blk ? (double)blk[j * gmax + j] : 1.0;
+        if (!(pii > 0.0 && pii <= 1.0 && pjj > 0.0 && pjj <= 1.0)) return ORC_ERHO;
+        *wi = 1.0 / pii;
+        *wj = 1.0 / pjj;
+    } else if (rule == ORC_RULE_UNWEIGHTED || rule == ORC_RULE_RATIO_KE) {
+        *wi = *wj = 1.0;
+    } else {
+        return ORC_EINVAL;
+    }
+    return ORC_OK;
+}
+
 /* ------------------------------------------------------------------------ */
-/* Induced-edge HT estimator, Eq. (pair-ht), one prompt, columns [0, D):     */
-/*   g = (1/M) sum_{i<j} (J_i J_j / rho_ij) h_ij,   M = G (G - 1) / 2.       */
-/* mask == NULL means every vertex completed; rho_blk == NULL means rho == 1 */
-/* (together: the complete-pair average of Eq. (pair-average)).             */
+/* One prompt's estimate under `rule`, columns [0, D), by explicit edges:    */
+/*   g = (1/N) sum_{i<j, J_i J_j = 1} 1/2 (r_i - r_j)(w_i s_i - w_j s_j);     */
+/* for the HT rule this is Eq. (pair-ht) with the edge kernel h_ij of        */
+/* Eq. (pair-kernel).  mask == NULL means every vertex completed; blk ==     */
+/* NULL means rho == 1 (with both: the complete-pair average, Eq.            */
+/* (pair-average)).  Optional: K_E, ESS and the largest edge weight.         */
 /* ------------------------------------------------------------------------ */
-static int ht_estimate_one(int64_t o, int64_t g, int64_t D, const void* scores, int dtype,
-                           int64_t ld, const float* rewards, const uint8_t* mask,
-                           const float* rho_blk, int32_t gmax, double* out, int32_t* edges) {
+static int rule_estimate_one(int64_t o, int64_t g, int64_t D, const void* scores, int dtype,
+                             int64_t ld, const float* rewards, const uint8_t* mask,
+                             const float* blk, int32_t gmax, int rule, double wmax, double* out,
+                             int32_t* edges, double* ess, double* maxw) {
     const double M = (double)g * (double)(g - 1) / 2.0;
     int32_t ke = 0;
+    double nsn = 0.0, sw = 0.0, sw2 = 0.0, wmx = 0.0;
     for (int64_t d = 0; d < D; ++d) out[d] = 0.0;
     for (int64_t i = 0; i < g; ++i) {
         for (int64_t j = i + 1; j < g; ++j) {
@@ -207,27 +263,54 @@ static int ht_estimate_one(int64_t o, int64_t g, int64_t D, const void* scores, 
             int Jj = mask ? mask[o + j] != 0 : 1;
             if (!(Ji && Jj)) continue; /* I_ij = 0: the edge is not observed */
             ++ke;
-            double rho = rho_blk ? rho_of(rho_blk, gmax, i, j) : 1.0;
-            if (!(rho > 0.0 && rho <= 1.0)) return ORC_ERHO;
+            double wi, wj, ir;
+            int st = edge_weights(rule, wmax, blk, gmax, i, j, &wi, &wj, &ir);
+            if (st) return st;
+            nsn += ir;
+            double we = 0.5 * (wi + wj);
+            sw += we;
+            sw2 += we * we;
+            if (we > wmx) wmx = we;
             double ri = (double)rewards[o + i], rj = (double)rewards[o + j];
             for (int64_t d = 0; d < D; ++d) {
                 double si = score_at(scores, dtype, ld, o + i, d);
                 double sj = score_at(scores, dtype, ld, o + j, d);
-                double h = 0.5 * (ri - rj) * (si - sj); /* Eq. (pair-kernel) */
-                out[d] += h / rho;
+                out[d] += 0.5 * (ri - rj) * (wi * si - wj * sj);
             }
         }
     }
-    for (int64_t d = 0; d < D; ++d) out[d] /= M;
+    double N = M;
+    if (rule == ORC_RULE_RATIO_KE) N = (double)ke;
+    if (rule == ORC_RULE_SELFNORM) N = nsn;
+    for (int64_t d = 0; d < D; ++d) out[d] = ke > 0 ? out[d] / N : 0.0;
     if (edges) *edges = ke;
+    if (ess) *ess = ke > 0 ? sw * sw / sw2 : 0.0;
+    if (maxw) *maxw = wmx;
     return ORC_OK;
 }
 
-/* Batched Eq. (pair-ht): out[b][d] for every prompt; edge_count[b] = K_E. */
-int orc_pair_grad(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D, const void* scores,
-                  int dtype, int64_t ld, const float* rewards, const uint8_t* mask, const float* pi,
-                  double* out, int32_t* edge_count) {
+static int ht_estimate_one(int64_t o, int64_t g, int64_t D, const void* scores, int dtype,
+                           int64_t ld, const float* rewards, const uint8_t* mask,
+                           const float* rho_blk, int32_t gmax, double* out, int32_t* edges) {
+    return rule_estimate_one(o, g, D, scores, dtype, ld, rewards, mask, rho_blk, gmax,
+                             ORC_RULE_HT, 0.0, out, edges, NULL, NULL);
+}
+
+static int check_rule(int rule, double wmax) {
+    if (rule < ORC_RULE_HT || rule > ORC_RULE_MARGINAL) return ORC_EINVAL;
+    if (rule == ORC_RULE_CLIPPED && !(wmax > 0.0 && wmax < INFINITY)) return ORC_EINVAL;
+    return ORC_OK;
+}
+
+/* Batched estimate under `rule`: out[b][d] for every prompt; optional
+ * edge_count[b] = K_E, ess[b], max_weight[b]. */
+int orc_pair_grad_rule(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D,
+                       const void* scores, int dtype, int64_t ld, const float* rewards,
+                       const uint8_t* mask, const float* pi, int rule, double wmax, double* out,
+                       int32_t* edge_count, double* ess, double* max_weight) {
     int st = check_offsets(B, offsets, gmax);
+    if (st) return st;
+    st = check_rule(rule, wmax);
     if (st) return st;
     if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_EDTYPE;
     if (D < 0 || ld < D || scores == NULL || rewards == NULL || out == NULL) return ORC_EINVAL;
@@ -236,8 +319,9 @@ int orc_pair_grad(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D, co
     for (int64_t b = 0; b < B; ++b) {
         int64_t o = offsets[b], g = offsets[b + 1] - offsets[b];
         const float* blk = pi ? pi + b * (int64_t)gmax * gmax : NULL;
-        int s = ht_estimate_one(o, g, D, scores, dtype, ld, rewards, mask, blk, gmax, out + b * D,
-                                edge_count ? edge_count + b : NULL);
+        int s = rule_estimate_one(o, g, D, scores, dtype, ld, rewards, mask, blk, gmax, rule, wmax,
+                                  out + b * D, edge_count ? edge_count + b : NULL,
+                                  ess ? ess + b : NULL, max_weight ? max_weight + b : NULL);
         if (s) {
 #pragma omp critical
             err = s;
@@ -246,20 +330,35 @@ int orc_pair_grad(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D, co
     return err;
 }
 
+/* Batched Eq. (pair-ht): out[b][d] for every prompt; edge_count[b] = K_E. */
+int orc_pair_grad(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D, const void* scores,
+                  int dtype, int64_t ld, const float* rewards, const uint8_t* mask, const float* pi,
+                  double* out, int32_t* edge_count) {
+    return orc_pair_grad_rule(B, offsets, gmax, D, scores, dtype, ld, rewards, mask, pi,
+                              ORC_RULE_HT, 0.0, out, edge_count, NULL, NULL);
+}
+
 /* ------------------------------------------------------------------------ */
 /* Sequence advantages, Eq. (pair-advantage), in the order of Algorithm 1:   */
-/* for every observed edge (i, j), i < j, the edge term h_ij / rho_ij puts   */
-/* (r_i - r_j) / (2 rho_ij) on s_i and its negative on s_j; divide by M.     */
+/* for every observed edge (i, j), i < j, the edge term puts                 */
+/* w_i (r_i - r_j) / 2 on s_i and -w_j (r_i - r_j) / 2 on s_j; divide by N.  */
+/* For the HT rule w = 1/rho and N = M.  No centring: in exact arithmetic    */
+/* the symmetric rules sum to zero already.                                  */
 /* ------------------------------------------------------------------------ */
-int orc_pair_coeffs(int64_t B, const int64_t* offsets, int32_t gmax, const float* rewards,
-                    const uint8_t* mask, const float* pi, double* coeff, int32_t* edge_count) {
+int orc_pair_coeffs_rule(int64_t B, const int64_t* offsets, int32_t gmax, const float* rewards,
+                         const uint8_t* mask, const float* pi, int rule, double wmax,
+                         double* coeff, int32_t* edge_count, double* ess, double* max_weight) {
     int st = check_offsets(B, offsets, gmax);
+    if (st) return st;
+    st = check_rule(rule, wmax);
     if (st) return st;
     if (rewards == NULL || coeff == NULL) return ORC_EINVAL;
     for (int64_t b = 0; b < B; ++b) {
         int64_t o = offsets[b], g = offsets[b + 1] - offsets[b];
+        const float* blk = pi ? pi + b * (int64_t)gmax * gmax : NULL;
         double M = (double)g * (double)(g - 1) / 2.0;
         int32_t ke = 0;
+        double nsn = 0.0, sw = 0.0, sw2 = 0.0, wmx = 0.0;
         for (int64_t i = 0; i < g; ++i) coeff[o + i] = 0.0;
         for (int64_t i = 0; i < g; ++i) {
             for (int64_t j = i + 1; j < g; ++j) {
@@ -267,34 +366,55 @@ int orc_pair_coeffs(int64_t B, const int64_t* offsets, int32_t gmax, const float
                 int Jj = mask ? mask[o + j] != 0 : 1;
                 if (!(Ji && Jj)) continue;
                 ++ke;
-                double rho = pi ? rho_of(pi + b * (int64_t)gmax * gmax, gmax, i, j) : 1.0;
-                if (!(rho > 0.0 && rho <= 1.0)) return ORC_ERHO;
-                double t = ((double)rewards[o + i] - (double)rewards[o + j]) / (2.0 * rho);
-                coeff[o + i] += t;
-                coeff[o + j] -= t;
+                double wi, wj, ir;
+                st = edge_weights(rule, wmax, blk, gmax, i, j, &wi, &wj, &ir);
+                if (st) return st;
+                nsn += ir;
+                double we = 0.5 * (wi + wj);
+                sw += we;
+                sw2 += we * we;
+                if (we > wmx) wmx = we;
+                double dr = (double)rewards[o + i] - (double)rewards[o + j];
+                coeff[o + i] += 0.5 * dr * wi;
+                coeff[o + j] -= 0.5 * dr * wj;
             }
         }
-        for (int64_t i = 0; i < g; ++i) coeff[o + i] /= M;
+        double N = M;
+        if (rule == ORC_RULE_RATIO_KE) N = (double)ke;
+        if (rule == ORC_RULE_SELFNORM) N = nsn;
+        for (int64_t i = 0; i < g; ++i) coeff[o + i] = ke > 0 ? coeff[o + i] / N : 0.0;
         if (edge_count) edge_count[b] = ke;
+        if (ess) ess[b] = ke > 0 ? sw * sw / sw2 : 0.0;
+        if (max_weight) max_weight[b] = wmx;
     }
     return ORC_OK;
+}
+
+int orc_pair_coeffs(int64_t B, const int64_t* offsets, int32_t gmax, const float* rewards,
+                    const uint8_t* mask, const float* pi, double* coeff, int32_t* edge_count) {
+    return orc_pair_coeffs_rule(B, offsets, gmax, rewards, mask, pi, ORC_RULE_HT, 0.0, coeff,
+                                edge_count, NULL, NULL);
 }
 
 /* ------------------------------------------------------------------------ */
 /* Frozen-population audit (Sec. 5.2, App. D).  For each prompt:             */
 /*   target  t   = complete-pair average, Eq. (pair-average)                 */
 /*   for r in [rep0, rep0 + R): draw J^(r) as orc_design_inclusion does,     */
-/*       g_r = Eq. (pair-ht) with weights 1/rho, rho = pi_w[b][i][j] when    */
-/*       pi_w is given, otherwise the logged fl32(p_i p_j);                  */
+/*       g_r = the estimate under `rule` (Eq. (pair-ht) for the HT rule),    */
+/*       rho = pi_w[b][i][j] when pi_w is given, otherwise the logged        */
+/*       fl32(p_i p_j) with p_i on the diagonal;                             */
 /*       e_r = || g_r - t ||^2                                               */
 /*   mse  = (1/R) sum_r e_r ;  bias = || (1/R) sum_r g_r - t ||              */
 /* rep_sqerr[b][R] and edge_count[b][R] are optional per-replicate outputs. */
 /* ------------------------------------------------------------------------ */
-int orc_audit(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D, const void* scores,
-              int dtype, int64_t ld, const float* rewards, const float* p, const float* pi_w,
-              uint64_t seed, int64_t rep0, int64_t R, const int64_t* prompt_id, double* mse,
-              double* bias_norm, double* rep_sqerr, int32_t* edge_count) {
+int orc_audit_rule(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D,
+                   const void* scores, int dtype, int64_t ld, const float* rewards,
+                   const float* p, const float* pi_w, int rule, double wmax, uint64_t seed,
+                   int64_t rep0, int64_t R, const int64_t* prompt_id, double* mse,
+                   double* bias_norm, double* rep_sqerr, int32_t* edge_count) {
     int st = check_offsets(B, offsets, gmax);
+    if (st) return st;
+    st = check_rule(rule, wmax);
     if (st) return st;
     if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_EDTYPE;
     if (D < 1 || ld < D || R < 1 || scores == NULL || rewards == NULL || p == NULL) return ORC_EINVAL;
@@ -320,7 +440,8 @@ int orc_audit(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D, const 
         } else {
             for (int64_t i = 0; s == ORC_OK && i < g; ++i)
                 for (int64_t j = 0; j < g; ++j)
-                    if (i != j) own[i * gmax + j] = (float)((double)p[o + i] * (double)p[o + j]);
+                    own[i * gmax + j] =
+                        i != j ? (float)((double)p[o + i] * (double)p[o + j]) : p[o + i];
         }
         if (s == ORC_OK)
             s = ht_estimate_one(o, g, D, scores, dtype, ld, rewards, NULL, NULL, gmax, t, NULL);
@@ -329,7 +450,8 @@ int orc_audit(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D, const 
             for (int64_t i = 0; i < g; ++i)
                 m[o + i] = (uint8_t)orc_draw_indicator(seed, rep0 + r, bid, i, p[o + i]);
             int32_t ke = 0;
-            s = ht_estimate_one(o, g, D, scores, dtype, ld, rewards, m, blk, gmax, gr, &ke);
+            s = rule_estimate_one(o, g, D, scores, dtype, ld, rewards, m, blk, gmax, rule, wmax, gr,
+                                  &ke, NULL, NULL);
             if (s) break;
             double e = 0.0;
             for (int64_t d = 0; d < D; ++d) {
@@ -356,6 +478,14 @@ int orc_audit(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D, const 
         free(t); free(gr); free(gsum); free(m); free(own);
     }
     return err;
+}
+
+int orc_audit(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D, const void* scores,
+              int dtype, int64_t ld, const float* rewards, const float* p, const float* pi_w,
+              uint64_t seed, int64_t rep0, int64_t R, const int64_t* prompt_id, double* mse,
+              double* bias_norm, double* rep_sqerr, int32_t* edge_count) {
+    return orc_audit_rule(B, offsets, gmax, D, scores, dtype, ld, rewards, p, pi_w, ORC_RULE_HT,
+                          0.0, seed, rep0, R, prompt_id, mse, bias_norm, rep_sqerr, edge_count);
 }
 
 /* Number of OpenMP threads the parallel loops above will use. */
