@@ -61,6 +61,29 @@ extern "C" {
 #define PAIR_ST_P_RANGE 4    /* a continuation probability outside (0, 1]      */
 #define PAIR_ST_NONFINITE 8  /* a non-finite score in an audited score block    */
 
+/* Edge-weight rules: the estimator variants compared in the paper's audit and
+ * ablation tables (Sec. 5, Tables 2, 4, 5; App. A "Naive selection bias" and
+ * App. B "Estimated and stabilized propensities").  Each rule estimates
+ *     g = (1/N) sum_{i<j observed} 1/2 (r_i - r_j) (w_i s_i - w_j s_j):
+ *   HT          w = 1/rho_ij,              N = M = C(G, 2)  exact PAIR, Eq. (pair-ht)
+ *   UNWEIGHTED  w = 1,                     N = M            naive selection
+ *   RATIO_KE    w = 1,                     N = K_E          mean over observed edges
+ *   CLIPPED     w = min(1/rho_ij, wmax),   N = M            stabilised weights
+ *   SELFNORM    w = 1/rho_ij,              N = sum over observed edges of 1/rho_ij
+ *   MARGINAL    w_i = 1/pi_i, w_j = 1/pi_j, N = M           per-rollout propensity only;
+ *               pi_i is the diagonal of the pi block (the paper names this
+ *               variant without a formula; this is the library's reading)
+ * HT, UNWEIGHTED and CLIPPED/SELFNORM coefficients are centred over the
+ * completed vertices (a rounding-level step: their folds sum to zero); the
+ * MARGINAL fold does not sum to zero and is not centred.  A prompt with fewer
+ * than two completed vertices gets exact zeros under every rule. */
+#define PAIR_RULE_HT 0
+#define PAIR_RULE_UNWEIGHTED 1
+#define PAIR_RULE_RATIO_KE 2
+#define PAIR_RULE_CLIPPED 3
+#define PAIR_RULE_SELFNORM 4
+#define PAIR_RULE_MARGINAL 5
+
 /* Largest group size supported by the design draw, the coefficient fold and
  * the audit (one 64-lane wavefront holds one prompt's vertices). */
 #define PAIR_GMAX_LIMIT 64
@@ -117,6 +140,29 @@ int pair_design_inclusion(int64_t B, int64_t nv, int32_t gmax, const int64_t* of
 int pair_edge_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                      const float* rewards, const uint8_t* mask, const float* pi, float* coeff,
                      int32_t* edge_count, int32_t* d_status, void* stream);
+
+/*
+ * pair_edge_coeffs_rule -- pair_edge_coeffs under any edge-weight rule
+ * (PAIR_RULE_*), plus the per-prompt weight diagnostics the paper logs
+ * (App. C "Probability optimization"; App. D metrics):
+ *     ess[b]        = (sum_e w_e)^2 / sum_e w_e^2 over the observed edges
+ *     max_weight[b] = max_e w_e
+ * with w_e the rule's edge weight ((w_i + w_j)/2 for MARGINAL); both are 0
+ * when fewer than two vertices completed.  pair_edge_coeffs is this call
+ * with PAIR_RULE_HT and no diagnostics.
+ *
+ *   rule           PAIR_RULE_* (anything else: PAIR_EINVAL)
+ *   wmax           weight cap for PAIR_RULE_CLIPPED (> 0, finite: else
+ *                  PAIR_EINVAL); ignored by the other rules
+ *   ess, max_weight  fp32 [B] out                                    (or NULL)
+ * Device status: as pair_edge_coeffs; PAIR_ST_RHO_RANGE also flags a
+ * marginal pi_i outside (0, 1] under PAIR_RULE_MARGINAL.  UNWEIGHTED and
+ * RATIO_KE read no rho.
+ */
+int pair_edge_coeffs_rule(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                          const float* rewards, const uint8_t* mask, const float* pi,
+                          int32_t rule, float wmax, float* coeff, int32_t* edge_count, float* ess,
+                          float* max_weight, int32_t* d_status, void* stream);
 
 /*
  * pair_weighted_grad -- the induced-edge HT gradient, paper Eq. (pair-ht)
@@ -184,6 +230,21 @@ int pair_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int6
                const float* p, const float* pi_w, uint64_t seed, int64_t rep0, int64_t R,
                double* mse, double* bias_norm, float* rep_sqerr, int32_t* edge_count,
                void* workspace, size_t ws_bytes, int32_t* d_status, void* stream);
+
+/*
+ * pair_audit_rule -- pair_audit replaying the estimator under an edge-weight
+ * rule (PAIR_RULE_*, wmax as in pair_edge_coeffs_rule) against the same
+ * complete-pair target: the audit matrix of the paper's Tables 2, 4 and 5
+ * (bias norm and MSE of each variant on a frozen population).  The marginal
+ * pi_i is the diagonal of pi_w when given, else p_i.  pair_audit is this call
+ * with PAIR_RULE_HT.
+ */
+int pair_audit_rule(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                    const void* scores, int32_t dtype, int64_t ld, const float* rewards,
+                    const float* p, const float* pi_w, int32_t rule, float wmax, uint64_t seed,
+                    int64_t rep0, int64_t R, double* mse, double* bias_norm, float* rep_sqerr,
+                    int32_t* edge_count, void* workspace, size_t ws_bytes, int32_t* d_status,
+                    void* stream);
 
 /* Human-readable text for a return code. */
 const char* pair_strerror(int code);

@@ -31,8 +31,16 @@ ST_P_RANGE = 4
 ST_NONFINITE = 8
 GMAX_LIMIT = 64
 
-EXPORTED = ("pair_design_inclusion", "pair_edge_coeffs", "pair_weighted_grad",
-            "pair_audit_workspace_bytes", "pair_audit", "pair_strerror", "pair_version")
+RULE_HT = 0
+RULE_UNWEIGHTED = 1
+RULE_RATIO_KE = 2
+RULE_CLIPPED = 3
+RULE_SELFNORM = 4
+RULE_MARGINAL = 5
+
+EXPORTED = ("pair_design_inclusion", "pair_edge_coeffs", "pair_edge_coeffs_rule",
+            "pair_weighted_grad", "pair_audit_workspace_bytes", "pair_audit", "pair_audit_rule",
+            "pair_strerror", "pair_version")
 
 
 class PairError(RuntimeError):
@@ -58,6 +66,12 @@ def lib() -> ctypes.CDLL:
         L.pair_design_inclusion.restype = ctypes.c_int
         L.pair_edge_coeffs.argtypes = [i64, i64, i32, P, P, P, P, P, P, P, P]
         L.pair_edge_coeffs.restype = ctypes.c_int
+        f32 = ctypes.c_float
+        L.pair_edge_coeffs_rule.argtypes = [i64, i64, i32, P, P, P, P, i32, f32, P, P, P, P, P, P]
+        L.pair_edge_coeffs_rule.restype = ctypes.c_int
+        L.pair_audit_rule.argtypes = [i64, i64, i32, P, i64, P, i32, i64, P, P, P, i32, f32, u64,
+                                      i64, i64, P, P, P, P, P, ctypes.c_size_t, P, P]
+        L.pair_audit_rule.restype = ctypes.c_int
         L.pair_weighted_grad.argtypes = [i64, i64, P, i64, P, i32, i64, P, P, i32, P, P]
         L.pair_weighted_grad.restype = ctypes.c_int
         L.pair_audit_workspace_bytes.argtypes = [i64, i32, i64, i64]
@@ -146,6 +160,18 @@ def pair_edge_coeffs(B, nv, gmax, offsets, rewards, mask, pi, coeff, edge_count=
         _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_edge_coeffs")
 
 
+def pair_edge_coeffs_rule(B, nv, gmax, offsets, rewards, mask, pi, rule, wmax, coeff,
+                          edge_count=None, ess=None, max_weight=None, d_status=None, stream=None):
+    _rc(lib().pair_edge_coeffs_rule(
+        B, nv, gmax, _dev(offsets, "offsets", torch.int64, B + 1),
+        _dev(rewards, "rewards", torch.float32, nv), _dev(mask, "mask", torch.uint8, nv, True),
+        _dev(pi, "pi", torch.float32, B * gmax * gmax, True), int(rule), float(wmax),
+        _dev(coeff, "coeff", torch.float32, nv),
+        _dev(edge_count, "edge_count", torch.int32, B, True),
+        _dev(ess, "ess", torch.float32, B, True), _dev(max_weight, "max_weight", torch.float32, B, True),
+        _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_edge_coeffs_rule")
+
+
 def pair_weighted_grad(B, nv, offsets, scores, coeff, out, reduce=0, d_status=None, stream=None):
     sp, code, ld, D = _scores_arg(scores)
     _rc(lib().pair_weighted_grad(
@@ -161,18 +187,28 @@ def pair_audit_workspace_bytes(B, gmax, D, R) -> int:
 
 def pair_audit(B, nv, gmax, offsets, scores, rewards, p, pi_w, seed, rep0, R, mse, bias_norm,
                rep_sqerr, edge_count, workspace, d_status=None, stream=None):
+    pair_audit_rule(B, nv, gmax, offsets, scores, rewards, p, pi_w, RULE_HT, 0.0, seed, rep0, R,
+                    mse, bias_norm, rep_sqerr, edge_count, workspace, d_status, stream,
+                    _name="pair_audit")
+
+
+def pair_audit_rule(B, nv, gmax, offsets, scores, rewards, p, pi_w, rule, wmax, seed, rep0, R,
+                    mse, bias_norm, rep_sqerr, edge_count, workspace, d_status=None, stream=None,
+                    _name="pair_audit_rule"):
     sp, code, ld, D = _scores_arg(scores)
     ws = _dev(workspace, "workspace", torch.uint8)
-    _rc(lib().pair_audit(
+    fn = lib().pair_audit if _name == "pair_audit" else lib().pair_audit_rule
+    extra = () if _name == "pair_audit" else (int(rule), float(wmax))
+    _rc(fn(
         B, nv, gmax, _dev(offsets, "offsets", torch.int64, B + 1), D, sp, code, ld,
         _dev(rewards, "rewards", torch.float32, nv), _dev(p, "p", torch.float32, nv),
-        _dev(pi_w, "pi_w", torch.float32, B * gmax * gmax, True),
+        _dev(pi_w, "pi_w", torch.float32, B * gmax * gmax, True), *extra,
         ctypes.c_uint64(seed & ((1 << 64) - 1)), rep0, R,
         _dev(mse, "mse", torch.float64, B), _dev(bias_norm, "bias_norm", torch.float64, B),
         _dev(rep_sqerr, "rep_sqerr", torch.float32, B * R, True),
         _dev(edge_count, "edge_count", torch.int32, B * R, True),
         ws, workspace.numel(), _dev(d_status, "d_status", torch.int32, 1, True),
-        _stream(stream)), "pair_audit")
+        _stream(stream)), _name)
 
 
 # ------------------------------------------------ allocating helpers -------
@@ -197,15 +233,22 @@ def design_inclusion(offsets, p, seed, rep0, R, gmax, want_mask=True, want_pi=Tr
     return out
 
 
-def edge_coeffs(offsets, rewards, mask, pi, gmax, nv=None, stream=None):
+def edge_coeffs(offsets, rewards, mask, pi, gmax, nv=None, rule=None, wmax=0.0, stream=None):
+    """Coefficients; with `rule` (RULE_*) also returns the ESS and the maximum weight."""
     B = offsets.numel() - 1
     nv = _nv(offsets) if nv is None else nv
     dev = rewards.device
     coeff = torch.empty(nv, dtype=torch.float32, device=dev)
     ec = torch.empty(B, dtype=torch.int32, device=dev)
     st = torch.zeros(1, dtype=torch.int32, device=dev)
-    pair_edge_coeffs(B, nv, gmax, offsets, rewards, mask, pi, coeff, ec, st, stream)
-    return {"coeff": coeff, "edge_count": ec, "status": st}
+    if rule is None:
+        pair_edge_coeffs(B, nv, gmax, offsets, rewards, mask, pi, coeff, ec, st, stream)
+        return {"coeff": coeff, "edge_count": ec, "status": st}
+    ess = torch.empty(B, dtype=torch.float32, device=dev)
+    mw = torch.empty(B, dtype=torch.float32, device=dev)
+    pair_edge_coeffs_rule(B, nv, gmax, offsets, rewards, mask, pi, rule, wmax, coeff, ec, ess, mw,
+                          st, stream)
+    return {"coeff": coeff, "edge_count": ec, "ess": ess, "max_weight": mw, "status": st}
 
 
 def weighted_grad(offsets, scores, coeff, nv=None, reduce=False, stream=None):
@@ -220,7 +263,7 @@ def weighted_grad(offsets, scores, coeff, nv=None, reduce=False, stream=None):
 
 
 def audit(offsets, scores, rewards, p, seed, rep0, R, gmax, pi_w=None, want_reps=True, nv=None,
-          workspace=None, stream=None):
+          workspace=None, rule=None, wmax=0.0, stream=None):
     B = offsets.numel() - 1
     nv = _nv(offsets) if nv is None else nv
     dev = scores.device
@@ -234,7 +277,12 @@ def audit(offsets, scores, rewards, p, seed, rep0, R, gmax, pi_w=None, want_reps
         "edge_count": torch.empty((B, R), dtype=torch.int32, device=dev) if want_reps else None,
         "status": torch.zeros(1, dtype=torch.int32, device=dev),
     }
-    pair_audit(B, nv, gmax, offsets, scores, rewards, p, pi_w, seed, rep0, R, out["mse"],
-               out["bias_norm"], out["rep_sqerr"], out["edge_count"], workspace, out["status"],
-               stream)
+    if rule is None:
+        pair_audit(B, nv, gmax, offsets, scores, rewards, p, pi_w, seed, rep0, R, out["mse"],
+                   out["bias_norm"], out["rep_sqerr"], out["edge_count"], workspace, out["status"],
+                   stream)
+    else:
+        pair_audit_rule(B, nv, gmax, offsets, scores, rewards, p, pi_w, rule, wmax, seed, rep0, R,
+                        out["mse"], out["bias_norm"], out["rep_sqerr"], out["edge_count"],
+                        workspace, out["status"], stream)
     return out

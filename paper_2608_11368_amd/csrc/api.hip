@@ -72,14 +72,30 @@ int pair_design_inclusion(int64_t B, int64_t nv, int32_t gmax, const int64_t* of
                              completed, d_status, as_stream(stream));
 }
 
+static int check_rule(int32_t rule, float wmax) {
+  if (rule < PAIR_RULE_HT || rule > PAIR_RULE_MARGINAL) return PAIR_EINVAL;
+  if (rule == PAIR_RULE_CLIPPED && !(wmax > 0.0f && wmax <= 3.4e38f)) return PAIR_EINVAL;
+  return PAIR_OK;
+}
+
+int pair_edge_coeffs_rule(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                          const float* rewards, const uint8_t* mask, const float* pi,
+                          int32_t rule, float wmax, float* coeff, int32_t* edge_count, float* ess,
+                          float* max_weight, int32_t* d_status, void* stream) {
+  int st = check_groups(B, nv, gmax, offsets);
+  if (st) return st;
+  st = check_rule(rule, wmax);
+  if (st) return st;
+  if (rewards == nullptr || coeff == nullptr) return PAIR_EINVAL;
+  return pair::launch_coeffs(B, nv, gmax, offsets, rewards, mask, pi, rule, wmax, coeff,
+                             edge_count, ess, max_weight, d_status, as_stream(stream));
+}
+
 int pair_edge_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                      const float* rewards, const uint8_t* mask, const float* pi, float* coeff,
                      int32_t* edge_count, int32_t* d_status, void* stream) {
-  int st = check_groups(B, nv, gmax, offsets);
-  if (st) return st;
-  if (rewards == nullptr || coeff == nullptr) return PAIR_EINVAL;
-  return pair::launch_coeffs(B, nv, gmax, offsets, rewards, mask, pi, coeff, edge_count, d_status,
-                             as_stream(stream));
+  return pair_edge_coeffs_rule(B, nv, gmax, offsets, rewards, mask, pi, PAIR_RULE_HT, 0.0f, coeff,
+                               edge_count, nullptr, nullptr, d_status, stream);
 }
 
 int pair_weighted_grad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D,
@@ -102,12 +118,15 @@ size_t pair_audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R)
   return pair::audit_workspace_bytes(B, gmax, D, R);
 }
 
-int pair_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
-               const void* scores, int32_t dtype, int64_t ld, const float* rewards,
-               const float* p, const float* pi_w, uint64_t seed, int64_t rep0, int64_t R,
-               double* mse, double* bias_norm, float* rep_sqerr, int32_t* edge_count,
-               void* workspace, size_t ws_bytes, int32_t* d_status, void* stream) {
+int pair_audit_rule(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                    const void* scores, int32_t dtype, int64_t ld, const float* rewards,
+                    const float* p, const float* pi_w, int32_t rule, float wmax, uint64_t seed,
+                    int64_t rep0, int64_t R, double* mse, double* bias_norm, float* rep_sqerr,
+                    int32_t* edge_count, void* workspace, size_t ws_bytes, int32_t* d_status,
+                    void* stream) {
   int st = check_groups(B, nv, gmax, offsets);
+  if (st) return st;
+  st = check_rule(rule, wmax);
   if (st) return st;
   if (dtype != PAIR_BF16) return PAIR_EDTYPE;
   st = check_scores(scores, dtype, D, ld);
@@ -120,9 +139,20 @@ int pair_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int6
   if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 ||
       ws_bytes < need)
     return PAIR_EWORKSPACE;
-  return pair::launch_audit(B, nv, gmax, offsets, D, scores, ld, rewards, p, pi_w, seed, rep0, R,
+  return pair::launch_audit(B, nv, gmax, offsets, D, scores, ld, rewards, p, pi_w, rule, wmax,
+                            seed, rep0, R,
                             mse, bias_norm, rep_sqerr, edge_count, workspace, d_status,
                             as_stream(stream));
+}
+
+int pair_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+               const void* scores, int32_t dtype, int64_t ld, const float* rewards,
+               const float* p, const float* pi_w, uint64_t seed, int64_t rep0, int64_t R,
+               double* mse, double* bias_norm, float* rep_sqerr, int32_t* edge_count,
+               void* workspace, size_t ws_bytes, int32_t* d_status, void* stream) {
+  return pair_audit_rule(B, nv, gmax, offsets, D, scores, dtype, ld, rewards, p, pi_w,
+                         PAIR_RULE_HT, 0.0f, seed, rep0, R, mse, bias_norm, rep_sqerr, edge_count,
+                         workspace, ws_bytes, d_status, stream);
 }
 
 const char* pair_strerror(int code) {

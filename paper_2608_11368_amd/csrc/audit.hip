@@ -108,11 +108,12 @@ template <int KP>
 __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets,
     const float* __restrict__ rewards, const float* __restrict__ p,
-    const float* __restrict__ pi_w, uint64_t seed, int64_t rep0, int64_t R, int64_t nwg,
-    int64_t rrows, float* __restrict__ delta, float* __restrict__ dsum,
+    const float* __restrict__ pi_w, int32_t rule, float wmax, uint64_t seed, int64_t rep0,
+    int64_t R, int64_t nwg, int64_t rrows, float* __restrict__ delta, float* __restrict__ dsum,
     int32_t* __restrict__ edge_count, int32_t* d_status) {
   constexpr int kWaves = kCoefThreads / kWave;
-  __shared__ __align__(16) float W[KP * KP];     // (r_i - r_j) / rho_ij, zero on and past G
+  __shared__ __align__(16) float W[KP * KP];     // rule weight x (r_i - r_j), zero on and past G
+  __shared__ __align__(16) float V[KP * KP];     // 1/rho_ij (self-normalised denominator)
   __shared__ float pl[KP], rl[KP], af[KP];
   __shared__ float wsum[kWaves][KP];
   const int64_t b = blockIdx.x / nwg;
@@ -149,22 +150,27 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
   bool bad_rho = false;
   for (int idx = tid; idx < KP * KP; idx += kCoefThreads) {
     const int i = idx / KP, j = idx - i * KP;
-    float w = 0.0f;
+    float w = 0.0f, v = 0.0f;
     if (i != j && i < g && j < g) {
-      float rho;
+      float rho, pii = pl[i], pij = pl[j];
       if (pi_w != nullptr) {
+        const float* blk = pi_w + b * (int64_t)gmax * gmax;
         const int lo = i < j ? i : j, hi = i < j ? j : i;
-        rho = pi_w[b * (int64_t)gmax * gmax + lo * gmax + hi];
+        rho = blk[lo * gmax + hi];
+        pii = blk[i * gmax + i];
+        pij = blk[j * gmax + j];
       } else {
         rho = pl[i] * pl[j];
       }
-      if (rho > 0.0f && rho <= 1.0f) {
-        w = (rl[i] - rl[j]) / rho;
-      } else {
+      float we;
+      if (!rule_term(rule, wmax, rl[i] - rl[j], rho, pii, pij, &w, &we, &v)) {
+        w = 0.0f;
+        v = 0.0f;
         bad_rho = true;
       }
     }
     W[idx] = w;
+    V[idx] = v;
   }
   if (bad_rho && chunk == 0) raise_status(d_status, PAIR_ST_RHO_RANGE);
   __syncthreads();
@@ -192,12 +198,32 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
   if (valid && edge_count != nullptr) edge_count[b * R + rloc] = k * (k - 1) / 2;
   if (k < 2) bits = 0;   // fewer than two completed vertices: A~ = 0
 
-  // Fold: A~_i = J_i (1/(G(G-1))) sum_j J_j W_ij, in ascending j; then centre
-  // over the completed vertices.
+  // Fold: A~_i = J_i (1/(2N)) sum_j J_j W_ij, in ascending j; then centre over
+  // the completed vertices (not for the marginal-only rule, whose fold is not
+  // antisymmetric).  2N = G (G - 1), or k (k - 1) for the observed-edge mean,
+  // or sum_{i, j observed} 1/rho_ij for the self-normalised rule.
   float m[KP], d[KP];
 #pragma unroll
   for (int j = 0; j < KP; ++j) m[j] = ((bits >> j) & 1ull) ? 1.0f : 0.0f;
-  const float den = (float)(g * (g - 1));
+  float den = (float)(g * (g - 1));
+  if (rule == PAIR_RULE_RATIO_KE) den = (float)(k * (k - 1));
+  if (rule == PAIR_RULE_SELFNORM) {
+    float n2 = 0.0f;
+#pragma unroll
+    for (int i = 0; i < KP; ++i) {
+      float c = 0.0f;
+#pragma unroll
+      for (int j0 = 0; j0 < KP; j0 += 4) {
+        const float4 v4 = *reinterpret_cast<const float4*>(&V[i * KP + j0]);
+        c = __builtin_fmaf(m[j0], v4.x, c);
+        c = __builtin_fmaf(m[j0 + 1], v4.y, c);
+        c = __builtin_fmaf(m[j0 + 2], v4.z, c);
+        c = __builtin_fmaf(m[j0 + 3], v4.w, c);
+      }
+      n2 = __builtin_fmaf(m[i], c, n2);
+    }
+    den = n2;
+  }
   float sum_obs = 0.0f;
 #pragma unroll
   for (int i = 0; i < KP; ++i) {
@@ -214,7 +240,7 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
     sum_obs += ai;
     d[i] = ai;
   }
-  const float mean = k >= 2 ? sum_obs / (float)k : 0.0f;
+  const float mean = (k >= 2 && rule != PAIR_RULE_MARGINAL) ? sum_obs / (float)k : 0.0f;
 #pragma unroll
   for (int i = 0; i < KP; ++i) d[i] = valid ? (m[i] != 0.0f ? d[i] - mean : 0.0f) - af[i] : 0.0f;
 
@@ -598,9 +624,9 @@ size_t audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R) {
 
 int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
                  const void* scores, int64_t ld, const float* rewards, const float* p,
-                 const float* pi_w, uint64_t seed, int64_t rep0, int64_t R, double* mse,
-                 double* bias_norm, float* rep_sqerr, int32_t* edge_count, void* workspace,
-                 int32_t* d_status, hipStream_t stream) {
+                 const float* pi_w, int32_t rule, float wmax, uint64_t seed, int64_t rep0,
+                 int64_t R, double* mse, double* bias_norm, float* rep_sqerr, int32_t* edge_count,
+                 void* workspace, int32_t* d_status, hipStream_t stream) {
   const AuditLayout L = audit_layout(B, gmax, D, R);
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   float* delta = reinterpret_cast<float*>(ws + L.delta_off);
@@ -614,8 +640,8 @@ int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, in
   if (coef_grid > 0x7fffffffLL) return PAIR_ERANGE;
 #define PAIR_AUDIT_COEFFS(KP_)                                                                  \
   hipLaunchKernelGGL(audit_coeffs_kernel<KP_>, dim3((unsigned)coef_grid), dim3(kCoefThreads), 0, \
-                     stream, B, nv, gmax, offsets, rewards, p, pi_w, seed, rep0, R, L.nwg,       \
-                     L.rrows, delta, dsum, edge_count, d_status)
+                     stream, B, nv, gmax, offsets, rewards, p, pi_w, rule, wmax, seed, rep0, R,  \
+                     L.nwg, L.rrows, delta, dsum, edge_count, d_status)
   switch (L.ks) {
     case 1: PAIR_AUDIT_COEFFS(16); break;
     case 2: PAIR_AUDIT_COEFFS(32); break;

@@ -3,6 +3,11 @@
 // finished as App. C describes (fp32 accumulation, centred over the observed
 // endpoints).
 //
+// The same fold serves the estimator variants of the audit and ablation
+// tables (edge-weight rules: unweighted, observed-edge mean, clipped,
+// self-normalised, marginal-only); it also reports the weights' effective
+// sample size (sum w)^2 / sum w^2 and the largest weight (App. D metrics).
+//
 // One 64-lane wavefront per prompt, lane i = vertex i.  The prompt's rho
 // block is staged in LDS (row stride gmax + 1 so that a column walk is
 // conflict-free); lane i then walks j = 0..G-1 in order and adds
@@ -13,10 +18,17 @@
 
 namespace pair {
 
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) v = fmaxf(v, __shfl_xor(v, m, kWave));
+  return v;
+}
+
 __global__ __launch_bounds__(64) void edge_coeffs_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets,
     const float* __restrict__ rewards, const uint8_t* __restrict__ mask,
-    const float* __restrict__ pi, float* __restrict__ coeff, int32_t* __restrict__ edge_count,
+    const float* __restrict__ pi, int32_t rule, float wmax, float* __restrict__ coeff,
+    int32_t* __restrict__ edge_count, float* __restrict__ ess, float* __restrict__ max_weight,
     int32_t* d_status) {
   extern __shared__ float rho_lds[];  // [gmax][gmax + 1]
   const int64_t b = blockIdx.x;
@@ -39,44 +51,65 @@ __global__ __launch_bounds__(64) void edge_coeffs_kernel(
   const float r_i = vert ? rewards[o0 + lane] : 0.0f;
   const uint64_t obs = __ballot(m_i);
   const int k = __popcll(obs);
+  const float pii = (pi != nullptr && vert) ? rho_lds[lane * stride + lane] : 1.0f;
 
-  float c = 0.0f;
+  float c = 0.0f, nsn = 0.0f, sw = 0.0f, sw2 = 0.0f, wmx = 0.0f;
   bool bad_rho = false;
   for (int j = 0; j < g; ++j) {
     const float r_j = __shfl(r_i, j, kWave);
     if (!((obs >> j) & 1ull) || !m_i || j == lane) continue;
-    float rho = 1.0f;
+    float rho = 1.0f, pij = 1.0f;
     if (pi != nullptr) {
       const int lo = lane < j ? lane : j, hi = lane < j ? j : lane;
       rho = rho_lds[lo * stride + hi];
+      pij = rho_lds[j * stride + j];
     }
-    if (!(rho > 0.0f && rho <= 1.0f)) {
+    float term, we, ir;
+    if (!rule_term(rule, wmax, r_i - r_j, rho, pii, pij, &term, &we, &ir)) {
       bad_rho = true;
       continue;
     }
-    c += (r_i - r_j) / rho;
+    c += term;
+    nsn += ir;
+    sw += we;
+    sw2 += we * we;
+    wmx = fmaxf(wmx, we);
   }
   if (bad_rho) raise_status(d_status, PAIR_ST_RHO_RANGE);
 
-  // A~_i = c_i / (2M), 2M = G (G - 1); centre over the completed vertices.
+  // A~_i = c_i / (2N): 2N = G (G - 1) for HT, unweighted, clipped and
+  // marginal-only; k (k - 1) for the observed-edge mean; sum over both
+  // endpoints of 1/rho for the self-normalised rule.  Centre over the
+  // completed vertices except for the marginal-only rule, whose fold is not
+  // antisymmetric.
+  float den = (float)(g * (g - 1));
+  if (rule == PAIR_RULE_RATIO_KE) den = (float)(k * (k - 1));
+  if (rule == PAIR_RULE_SELFNORM) den = wave_sum(nsn);
   float a = 0.0f;
-  if (m_i && k >= 2) a = c / (float)(g * (g - 1));
-  const float total = wave_sum(a);
-  if (k >= 2 && m_i) {
-    a = a - total / (float)k;
-  } else {
-    a = 0.0f;
+  if (m_i && k >= 2) a = c / den;
+  if (rule != PAIR_RULE_MARGINAL) {
+    const float total = wave_sum(a);
+    if (k >= 2 && m_i) a = a - total / (float)k;
   }
+  if (!(k >= 2 && m_i)) a = 0.0f;
   if (vert) coeff[o0 + lane] = a;
-  if (lane == 0 && edge_count != nullptr) edge_count[b] = k * (k - 1) / 2;
+  // Every edge was visited from both endpoints: (S/2)^2 / (S2/2) = S^2 / (2 S2).
+  const float s1 = wave_sum(sw), s2 = wave_sum(sw2), mx = wave_max(wmx);
+  if (lane == 0) {
+    if (edge_count != nullptr) edge_count[b] = k * (k - 1) / 2;
+    if (ess != nullptr) ess[b] = k >= 2 ? s1 * s1 / (2.0f * s2) : 0.0f;
+    if (max_weight != nullptr) max_weight[b] = k >= 2 ? mx : 0.0f;
+  }
 }
 
 int launch_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
-                  const float* rewards, const uint8_t* mask, const float* pi, float* coeff,
-                  int32_t* edge_count, int32_t* d_status, hipStream_t stream) {
+                  const float* rewards, const uint8_t* mask, const float* pi, int32_t rule,
+                  float wmax, float* coeff, int32_t* edge_count, float* ess, float* max_weight,
+                  int32_t* d_status, hipStream_t stream) {
   const size_t lds = pi != nullptr ? (size_t)gmax * (gmax + 1) * sizeof(float) : 0;
   hipLaunchKernelGGL(edge_coeffs_kernel, dim3((unsigned)B), dim3(64), lds, stream, B, nv, gmax,
-                     offsets, rewards, mask, pi, coeff, edge_count, d_status);
+                     offsets, rewards, mask, pi, rule, wmax, coeff, edge_count, ess, max_weight,
+                     d_status);
   return hipGetLastError() == hipSuccess ? PAIR_OK : PAIR_EHIP;
 }
 

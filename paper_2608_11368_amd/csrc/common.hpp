@@ -96,6 +96,40 @@ __device__ __forceinline__ void raise_status(int32_t* d_status, int32_t bits) {
   if (d_status != nullptr) atomicOr(d_status, bits);
 }
 
+// Edge weight on vertex i's half of observed edge (i, j) under `rule`
+// (PAIR_RULE_*), applied to dr = r_i - r_j; also the edge's own weight (for ESS and the maximum) and
+// its share 1/rho of the self-normalised denominator.  Returns false when the
+// rule needs rho (or the marginals) and they are outside (0, 1].
+__device__ __forceinline__ bool rule_term(int rule, float wmax, float dr, float rho, float pii,
+                                          float pij, float* term, float* w_edge, float* inv_rho) {
+  *inv_rho = 0.0f;
+  switch (rule) {
+    case PAIR_RULE_UNWEIGHTED:
+    case PAIR_RULE_RATIO_KE:
+      *term = dr;
+      *w_edge = 1.0f;
+      return true;
+    case PAIR_RULE_MARGINAL:
+      if (!(p_in_range(pii) && p_in_range(pij))) return false;
+      *term = dr / pii;
+      *w_edge = 0.5f * (1.0f / pii + 1.0f / pij);
+      return true;
+    default: {  // HT, CLIPPED, SELFNORM
+      if (!(rho > 0.0f && rho <= 1.0f)) return false;
+      const float w = 1.0f / rho;
+      *inv_rho = w;
+      if (rule == PAIR_RULE_CLIPPED && w > wmax) {
+        *term = dr * wmax;
+        *w_edge = wmax;
+      } else {
+        *term = dr / rho;
+        *w_edge = w;
+      }
+      return true;
+    }
+  }
+}
+
 // Validated bounds of prompt b: returns false (and sets the status bit) when
 // the offsets are not monotone, leave [0, nv], or G_b is outside [gmin, gmax].
 __device__ __forceinline__ bool prompt_bounds(const int64_t* offsets, int64_t b, int64_t nv,

@@ -16,8 +16,9 @@ int launch_design(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, c
                   int32_t* edge_count, int32_t* completed, int32_t* d_status, hipStream_t stream);
 
 int launch_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
-                  const float* rewards, const uint8_t* mask, const float* pi, float* coeff,
-                  int32_t* edge_count, int32_t* d_status, hipStream_t stream);
+                  const float* rewards, const uint8_t* mask, const float* pi, int32_t rule,
+                  float wmax, float* coeff, int32_t* edge_count, float* ess, float* max_weight,
+                  int32_t* d_status, hipStream_t stream);
 
 int launch_wgrad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D, const void* scores,
                  int32_t dtype, int64_t ld, const float* coeff, float* out, int32_t reduce,
@@ -27,7 +28,8 @@ size_t audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R);
 
 int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
                  const void* scores, int64_t ld, const float* rewards, const float* p,
-                 const float* pi_w, uint64_t seed, int64_t rep0, int64_t R, double* mse,
+                 const float* pi_w, int32_t rule, float wmax, uint64_t seed, int64_t rep0,
+                 int64_t R, double* mse,
                  double* bias_norm, float* rep_sqerr, int32_t* edge_count, void* workspace,
                  int32_t* d_status, hipStream_t stream);
 

@@ -126,3 +126,30 @@ def test_binding_checks_tensors_before_calling():
     t = torch.zeros(4)
     with pytest.raises(ValueError):
         pair._dev(t, "x", torch.float32)          # host tensor is refused
+
+
+def test_rule_entry_points_reject_bad_rules():
+    L = pair.lib()
+    f = L.pair_edge_coeffs_rule
+
+    def call(rule=0, wmax=0.0, rewards=FAKE, coeff=FAKE):
+        return f(4, 32, 8, FAKE, rewards, NULL, NULL, rule, wmax, coeff, NULL, NULL, NULL, NULL,
+                 NULL)
+
+    assert call(rule=6) == -1
+    assert call(rule=-1) == -1
+    assert call(rule=pair.RULE_CLIPPED, wmax=0.0) == -1
+    assert call(rule=pair.RULE_CLIPPED, wmax=-2.0) == -1
+    assert call(rule=pair.RULE_CLIPPED, wmax=float("inf")) == -1
+    assert call(rule=pair.RULE_CLIPPED, wmax=float("nan")) == -1
+    assert call(rewards=NULL) == -1
+    assert call(coeff=NULL) == -1
+    need = L.pair_audit_workspace_bytes(4, 8, 64, 10)
+    g = L.pair_audit_rule
+
+    def acall(rule=0, wmax=0.0):
+        return g(4, 32, 8, FAKE, 64, FAKE, 1, 64, FAKE, FAKE, NULL, rule, wmax, 1, 0, 10, FAKE,
+                 FAKE, NULL, NULL, FAKE, need, NULL, NULL)
+
+    assert acall(rule=7) == -1
+    assert acall(rule=pair.RULE_CLIPPED, wmax=0.0) == -1
