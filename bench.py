@@ -197,6 +197,53 @@ def cpu_baseline(meta, w, scores_dev, meta_a, wa, scores_a_dev, budget_s=12.0):
     }
 
 
+RULE_NAMES = ("ht", "unweighted", "ratio_ke", "clipped", "selfnorm", "marginal")
+
+
+def time_variants(pair, stream, B, nv, G, off, rew, mask, pi, coeff, audit_args, status, reps=5):
+    """Estimator variants (edge-weight rules): the coefficient fold on the
+    b128 draw and the audit replay on the audit workload, per rule, timed
+    with events on the launch stream (outside the main timed steps)."""
+    import torch
+
+    Ba, nva, Ga, off_a, scores_a, rew_a, p_a, wa, R, mse, bias, rps, ec_a, ws = audit_args
+    dev = coeff.device
+    ess = torch.empty(B, dtype=torch.float32, device=dev)
+    mw = torch.empty(B, dtype=torch.float32, device=dev)
+    out = {}
+    with torch.cuda.stream(stream):
+        for rule, name in enumerate(RULE_NAMES):
+            wmax = 10.0 if name == "clipped" else 0.0
+
+            def coeffs():
+                pair.pair_edge_coeffs_rule(B, nv, G, off, rew, mask[0], pi, rule, wmax, coeff, None,
+                                           ess, mw, status, stream)
+
+            def audit():
+                pair.pair_audit_rule(Ba, nva, Ga, off_a, scores_a, rew_a, p_a, None, rule, wmax,
+                                     wa.design_seed, 0, R, mse, bias, rps, ec_a, ws, status, stream)
+
+            res = {}
+            for key, fn in (("coeffs_us", coeffs), ("audit_ms", audit)):
+                fn()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(reps):
+                    fn()
+                e1.record(stream)
+                e1.synchronize()
+                t = e0.elapsed_time(e1) / reps
+                res[key] = round(t * 1e3 if key == "coeffs_us" else t, 4)
+            res["audit_mean_mse"] = float(mse.mean().item())
+            res["audit_mean_bias"] = float(bias.mean().item())
+            res["b128_mean_ess"] = round(float(ess.mean().item()), 3)
+            out[name] = res
+    if int(status.item()) != 0:
+        raise RuntimeError(f"device status {int(status.item())} in the variant timings")
+    return out
+
+
 def copy_calibration(gib=1.0, reps=5):
     """Plain device copy of known size, for scaling rocprofv3 FETCH/WRITE
     counters, timed with events; also a read-only reduction over a 4x larger
@@ -378,6 +425,9 @@ def main():
         "audit": {"value": round(Ba * R / (ms_audit * 1e-3), 1),
                   "unit": "replicate-estimates/s", "roofline": roof_a},
     }
+    result["variants"] = time_variants(pair, stream, B, nv, G, off, rew, mask, pi, coeff,
+                                       (Ba, nva, Ga, off_a, scores_a, rew_a, p_a, wa, R, mse, bias,
+                                        reps, ec_a, ws), status)
     if not args.no_cpu_baseline:
         _log("[bench] timing the CPU oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(meta, w, scores, meta_a, wa, scores_a)
