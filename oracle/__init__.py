@@ -18,6 +18,10 @@ Parity status of each function (what pins it, see ``tests/test_oracle_pins.py``)
   audit             pinned: exact design covariance trace (Prop 1) by
                     enumeration; Gram-matrix identity for every replicate;
                     bias^2 ~ MSE/R statistics; p == 1 gives zero MSE
+  audit_exact       pinned: exhaustive design enumeration of E||g^ - t||^2 and
+                    of the mean for every linear rule; zero bias for HT
+                    (Thm 2); Prop. 1's unweighted bias vector; zero error
+                    when p == 1
   *_rule variants   pinned by exhaustive design enumeration against the
                     expectations the paper states for each edge-weight rule
                     (naive bias, clipped multiplier min(1, w_max rho) - 1,
@@ -108,6 +112,9 @@ def _load():
         lib.orc_audit_rule.argtypes = [i64, P, i32, i64, P, ctypes.c_int, i64, P, P, P,
                                        ctypes.c_int, dbl, u64, i64, i64, P, P, P, P, P]
         lib.orc_audit_rule.restype = ctypes.c_int
+        lib.orc_audit_exact.argtypes = [i64, P, i32, i64, P, ctypes.c_int, i64, P, P, P,
+                                        ctypes.c_int, dbl, P, P]
+        lib.orc_audit_exact.restype = ctypes.c_int
         lib.orc_num_threads.argtypes = []
         lib.orc_num_threads.restype = ctypes.c_int
         _lib = lib
@@ -291,3 +298,24 @@ def audit(offsets, scores, rewards, p, seed, rep0, R, pi_w=None, gmax=None, prom
                               _ptr(pi_w), int(rule), float(wmax), seed, rep0, R, _ptr(pid),
                               _ptr(mse), _ptr(bias), _ptr(reps), _ptr(ec)))
     return {"mse": mse, "bias_norm": bias, "rep_sqerr": reps, "edge_count": ec}
+
+
+def audit_exact(offsets, scores, rewards, p, pi_w=None, gmax=None, rule=RULE_HT, wmax=0.0):
+    """Exact design MSE and bias norm per prompt (Prop. 1), no draws, for the
+    linear rules (HT, unweighted, clipped, marginal-only).  Returns
+    dict(mse[B], bias_norm[B])."""
+    lib = _load()
+    off = _offsets(offsets)
+    B = off.size - 1
+    s, code, ld = _scores_arg(scores)
+    D = s.shape[1]
+    r = np.ascontiguousarray(rewards, dtype=np.float32)
+    pp = np.ascontiguousarray(p, dtype=np.float32)
+    if pi_w is not None:
+        pi_w = np.ascontiguousarray(pi_w, dtype=np.float32)
+    gmax = _gmax(off, pi_w, gmax)
+    mse = np.zeros(B, dtype=np.float64)
+    bias = np.zeros(B, dtype=np.float64)
+    _check(lib.orc_audit_exact(B, _ptr(off), gmax, D, _ptr(s), code, ld, _ptr(r), _ptr(pp),
+                               _ptr(pi_w), int(rule), float(wmax), _ptr(mse), _ptr(bias)))
+    return {"mse": mse, "bias_norm": bias}

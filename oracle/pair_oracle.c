@@ -29,6 +29,8 @@
  *   - App. A "Naive selection bias" and App. B "Estimated and stabilized
  *     propensities": the estimator variants of Tables 4 and 5 (edge-weight
  *     rules, below)
+ *   - Prop. 1 and App. A "Design covariance": the exact design bias and
+ *     covariance trace of a linear rule (orc_audit_exact)
  *
  * Random design draws.  The paper only requires fresh randomisation for the
  * continuation indicators.  This oracle fixes one counter-based generator, the
@@ -486,6 +488,115 @@ int orc_audit(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D, const 
               double* bias_norm, double* rep_sqerr, int32_t* edge_count) {
     return orc_audit_rule(B, offsets, gmax, D, scores, dtype, ld, rewards, p, pi_w, ORC_RULE_HT,
                           0.0, seed, rep0, R, prompt_id, mse, bias_norm, rep_sqerr, edge_count);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Exact design audit (Prop. 1 and App. A "Design covariance"), no draws.    */
+/* For a rule that is linear in the edge indicators (HT, UNWEIGHTED,         */
+/* CLIPPED, MARGINAL), g^ = (1/M) sum_e I_e v_e with the edge vectors        */
+/*     v_ij = 1/2 (r_i - r_j) (w_i s_i - w_j s_j)                            */
+/* (weights from the logged rho: pi_w when given, else fl32(p_i p_j), p_i    */
+/* on the diagonal).  Under the true design, independent Bernoulli(p_i)      */
+/* vertices with rho_e = p_i p_j (exact fp64 products):                      */
+/*     E g^ = (1/M) sum_e rho_e v_e,   bias = || E g^ - t ||,                */
+/*     tr Cov g^ = (1/M^2) [ sum_e rho_e (1 - rho_e) ||v_e||^2               */
+/*        + sum_i sum_{j != k, both != i} p_i p_j p_k (1 - p_i) <v_ij, v_ik> ]*/
+/* (the shared-vertex covariance of I_ij and I_ik, over ordered pairs), and  */
+/*     mse = bias^2 + tr Cov = E || g^ - t ||^2,                             */
+/* with t the complete-pair average.  Every vector is formed explicitly.     */
+/* ------------------------------------------------------------------------ */
+int orc_audit_exact(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D,
+                    const void* scores, int dtype, int64_t ld, const float* rewards,
+                    const float* p, const float* pi_w, int rule, double wmax, double* mse,
+                    double* bias_norm) {
+    int st = check_offsets(B, offsets, gmax);
+    if (st) return st;
+    st = check_rule(rule, wmax);
+    if (st) return st;
+    if (rule == ORC_RULE_RATIO_KE || rule == ORC_RULE_SELFNORM) return ORC_EINVAL;
+    if (dtype != ORC_F32 && dtype != ORC_BF16) return ORC_EDTYPE;
+    if (D < 1 || ld < D || scores == NULL || rewards == NULL || p == NULL) return ORC_EINVAL;
+    if (gmax < 2) return ORC_EINVAL;
+    int64_t nv = offsets[B];
+    for (int64_t v = 0; v < nv; ++v)
+        if (!(p[v] > 0.0f && p[v] <= 1.0f)) return ORC_EP;
+    int err = ORC_OK;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        int64_t o = offsets[b], g = offsets[b + 1] - offsets[b];
+        double M = (double)g * (double)(g - 1) / 2.0;
+        double* v = (double*)calloc((size_t)(g * g * D), sizeof(double)); /* v[(i*g+j)*D] */
+        double* t = (double*)calloc((size_t)D, sizeof(double));
+        double* mu = (double*)calloc((size_t)D, sizeof(double));
+        float* own = (float*)calloc((size_t)gmax * gmax, sizeof(float));
+        int s = (v && t && mu && own) ? ORC_OK : ORC_EINVAL;
+        const float* blk = own;
+        if (pi_w) {
+            blk = pi_w + b * (int64_t)gmax * gmax;
+        } else {
+            for (int64_t i = 0; i < g; ++i)
+                for (int64_t j = 0; j < g; ++j)
+                    own[i * gmax + j] =
+                        i != j ? (float)((double)p[o + i] * (double)p[o + j]) : p[o + i];
+        }
+        /* edge vectors, both orientations (v_ij = v_ji), and the target */
+        for (int64_t i = 0; s == ORC_OK && i < g; ++i) {
+            for (int64_t j = i + 1; j < g; ++j) {
+                double wi, wj, ir;
+                s = edge_weights(rule, wmax, blk, gmax, i, j, &wi, &wj, &ir);
+                if (s) break;
+                double dr = (double)rewards[o + i] - (double)rewards[o + j];
+                double* vij = v + (i * g + j) * D;
+                double* vji = v + (j * g + i) * D;
+                for (int64_t d = 0; d < D; ++d) {
+                    double si = score_at(scores, dtype, ld, o + i, d);
+                    double sj = score_at(scores, dtype, ld, o + j, d);
+                    vij[d] = 0.5 * dr * (wi * si - wj * sj);
+                    vji[d] = vij[d];
+                    t[d] += 0.5 * dr * (si - sj) / M;
+                }
+            }
+        }
+        double tr = 0.0, bb = 0.0;
+        if (s == ORC_OK) {
+            for (int64_t i = 0; i < g; ++i) {
+                double pi_ = (double)p[o + i];
+                for (int64_t j = 0; j < g; ++j) {
+                    if (j == i) continue;
+                    double pj = (double)p[o + j];
+                    const double* vij = v + (i * g + j) * D;
+                    if (j > i) {
+                        double rho = pi_ * pj, nn = 0.0;
+                        for (int64_t d = 0; d < D; ++d) {
+                            mu[d] += rho * vij[d] / M;
+                            nn += vij[d] * vij[d];
+                        }
+                        tr += rho * (1.0 - rho) * nn;
+                    }
+                    for (int64_t k = 0; k < g; ++k) {
+                        if (k == i || k == j) continue;
+                        double pk = (double)p[o + k];
+                        const double* vik = v + (i * g + k) * D;
+                        double ip = 0.0;
+                        for (int64_t d = 0; d < D; ++d) ip += vij[d] * vik[d];
+                        tr += pi_ * pj * pk * (1.0 - pi_) * ip;
+                    }
+                }
+            }
+            tr /= M * M;
+            for (int64_t d = 0; d < D; ++d) {
+                double e = mu[d] - t[d];
+                bb += e * e;
+            }
+            mse[b] = bb + tr;
+            bias_norm[b] = sqrt(bb);
+        } else {
+#pragma omp critical
+            err = s;
+        }
+        free(v); free(t); free(mu); free(own);
+    }
+    return err;
 }
 
 /* Number of OpenMP threads the parallel loops above will use. */
