@@ -200,6 +200,42 @@ def cpu_baseline(meta, w, scores_dev, meta_a, wa, scores_a_dev, budget_s=12.0):
 RULE_NAMES = ("ht", "unweighted", "ratio_ke", "clipped", "selfnorm", "marginal")
 
 
+def time_exact_audit(pair, stream, B, nv, G, off, scores, rew, p, D, reps=10):
+    """Exact design audit (Gram on the matrix cores + closed form) on the
+    audit workload, timed with events on the launch stream.  HBM-bound: the
+    algorithmic bytes are the score block read once."""
+    import torch
+
+    dev = scores.device
+    ws = torch.empty(pair.pair_audit_exact_workspace_bytes(B, G, D), dtype=torch.uint8, device=dev)
+    mse = torch.empty(B, dtype=torch.float64, device=dev)
+    bias = torch.empty(B, dtype=torch.float64, device=dev)
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+    with torch.cuda.stream(stream):
+        def run():
+            pair.pair_audit_exact(B, nv, G, off, scores, rew, p, None, 0, 0.0, mse, bias, None, ws,
+                                  st, stream)
+        run()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            run()
+        e1.record(stream)
+        e1.synchronize()
+    if int(st.item()) != 0:
+        raise RuntimeError(f"device status {int(st.item())} in the exact audit")
+    ms = e0.elapsed_time(e1) / reps
+    nbytes = nv * D * 2
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    return {"ms": round(ms, 4), "prompts_per_s": round(B / (ms * 1e-3), 1),
+            "mean_mse": float(mse.mean().item()),
+            "roofline": {"kernel": "gram_kernel + exact_final_kernel (pair_audit_exact)",
+                         "bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS,
+                         "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                         "algorithmic_bytes": nbytes}}
+
+
 def time_variants(pair, stream, B, nv, G, off, rew, mask, pi, coeff, audit_args, status, reps=5):
     """Estimator variants (edge-weight rules): the coefficient fold on the
     b128 draw and the audit replay on the audit workload, per rule, timed
@@ -425,6 +461,8 @@ def main():
         "audit": {"value": round(Ba * R / (ms_audit * 1e-3), 1),
                   "unit": "replicate-estimates/s", "roofline": roof_a},
     }
+    result["exact_audit"] = time_exact_audit(pair, stream, Ba, nva, Ga, off_a, scores_a, rew_a,
+                                             p_a, Da)
     result["variants"] = time_variants(pair, stream, B, nv, G, off, rew, mask, pi, coeff,
                                        (Ba, nva, Ga, off_a, scores_a, rew_a, p_a, wa, R, mse, bias,
                                         reps, ec_a, ws), status)

@@ -246,6 +246,47 @@ int pair_audit_rule(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                     int32_t* edge_count, void* workspace, size_t ws_bytes, int32_t* d_status,
                     void* stream);
 
+/*
+ * pair_audit_exact_workspace_bytes -- device workspace that pair_audit_exact
+ * needs for B prompts of at most gmax vertices and D score columns.
+ */
+size_t pair_audit_exact_workspace_bytes(int64_t B, int32_t gmax, int64_t D);
+
+/*
+ * pair_audit_exact -- the exact design audit, with no replicate draws (paper
+ * Prop. 1 and App. A "Design covariance"): for an estimator that is linear in
+ * the edge indicators, g^ = (1/M) sum_e I_e v_e with
+ * v_ij = 1/2 (r_i - r_j)(w_i s_i - w_j s_j), under independent Bernoulli(p_i)
+ * vertices (rho_ij = p_i p_j),
+ *     bias = || E g^ - t ||,
+ *     mse  = bias^2 + tr Cov g^
+ *          = bias^2 + (1/M^2) [ sum_{i<j} rho_ij (1 - rho_ij) ||v_ij||^2
+ *            + sum_i sum_{j != k; j, k != i} p_i p_j p_k (1 - p_i) <v_ij, v_ik> ]
+ * with t the complete-pair average, i.e. mse = E || g^ - t ||^2 exactly (the
+ * limit of pair_audit's Monte-Carlo mse as R grows; for the HT rule bias = 0,
+ * Theorem 2).  Every inner product is taken from the prompt's Gram matrix
+ * K = S_b S_b^T, formed on the matrix cores (bf16 products, fp32 partial sums
+ * per column slice, fp64 across slices); the closed form is evaluated in fp64.
+ *
+ *   rule, wmax     PAIR_RULE_HT, _UNWEIGHTED, _CLIPPED or _MARGINAL (the rules
+ *                  linear in the indicators; others: PAIR_EINVAL); the
+ *                  weights use pi_w when given, else the logged fl32(p_i p_j)
+ *                  with p_i as the marginal; the design itself is p
+ *   scores, dtype  PAIR_BF16 only
+ *   mse, bias_norm fp64 [B] out
+ *   gram           fp64 [B][gmax][gmax] out: K_ij for i, j < G_b (other
+ *                  entries untouched)                             (or NULL)
+ *   workspace      device scratch of ws_bytes >=
+ *                  pair_audit_exact_workspace_bytes, 256-byte aligned
+ * Device status: PAIR_ST_BAD_GROUP, PAIR_ST_P_RANGE, PAIR_ST_RHO_RANGE,
+ * PAIR_ST_NONFINITE (a non-finite Gram entry).
+ */
+int pair_audit_exact(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                     const void* scores, int32_t dtype, int64_t ld, const float* rewards,
+                     const float* p, const float* pi_w, int32_t rule, float wmax, double* mse,
+                     double* bias_norm, double* gram, void* workspace, size_t ws_bytes,
+                     int32_t* d_status, void* stream);
+
 /* Human-readable text for a return code. */
 const char* pair_strerror(int code);
 

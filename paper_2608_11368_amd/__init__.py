@@ -40,7 +40,8 @@ RULE_MARGINAL = 5
 
 EXPORTED = ("pair_design_inclusion", "pair_edge_coeffs", "pair_edge_coeffs_rule",
             "pair_weighted_grad", "pair_audit_workspace_bytes", "pair_audit", "pair_audit_rule",
-            "pair_strerror", "pair_version")
+            "pair_audit_exact_workspace_bytes", "pair_audit_exact", "pair_strerror",
+            "pair_version")
 
 
 class PairError(RuntimeError):
@@ -72,6 +73,11 @@ def lib() -> ctypes.CDLL:
         L.pair_audit_rule.argtypes = [i64, i64, i32, P, i64, P, i32, i64, P, P, P, i32, f32, u64,
                                       i64, i64, P, P, P, P, P, ctypes.c_size_t, P, P]
         L.pair_audit_rule.restype = ctypes.c_int
+        L.pair_audit_exact_workspace_bytes.argtypes = [i64, i32, i64]
+        L.pair_audit_exact_workspace_bytes.restype = ctypes.c_size_t
+        L.pair_audit_exact.argtypes = [i64, i64, i32, P, i64, P, i32, i64, P, P, P, i32, f32, P, P,
+                                       P, P, ctypes.c_size_t, P, P]
+        L.pair_audit_exact.restype = ctypes.c_int
         L.pair_weighted_grad.argtypes = [i64, i64, P, i64, P, i32, i64, P, P, i32, P, P]
         L.pair_weighted_grad.restype = ctypes.c_int
         L.pair_audit_workspace_bytes.argtypes = [i64, i32, i64, i64]
@@ -211,6 +217,23 @@ def pair_audit_rule(B, nv, gmax, offsets, scores, rewards, p, pi_w, rule, wmax, 
         _stream(stream)), _name)
 
 
+def pair_audit_exact_workspace_bytes(B, gmax, D) -> int:
+    return int(lib().pair_audit_exact_workspace_bytes(B, gmax, D))
+
+
+def pair_audit_exact(B, nv, gmax, offsets, scores, rewards, p, pi_w, rule, wmax, mse, bias_norm,
+                     gram, workspace, d_status=None, stream=None):
+    sp, code, ld, D = _scores_arg(scores)
+    _rc(lib().pair_audit_exact(
+        B, nv, gmax, _dev(offsets, "offsets", torch.int64, B + 1), D, sp, code, ld,
+        _dev(rewards, "rewards", torch.float32, nv), _dev(p, "p", torch.float32, nv),
+        _dev(pi_w, "pi_w", torch.float32, B * gmax * gmax, True), int(rule), float(wmax),
+        _dev(mse, "mse", torch.float64, B), _dev(bias_norm, "bias_norm", torch.float64, B),
+        _dev(gram, "gram", torch.float64, B * gmax * gmax, True),
+        _dev(workspace, "workspace", torch.uint8), workspace.numel(),
+        _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_audit_exact")
+
+
 # ------------------------------------------------ allocating helpers -------
 def _nv(offsets):
     return int(offsets[-1].item())
@@ -285,4 +308,24 @@ def audit(offsets, scores, rewards, p, seed, rep0, R, gmax, pi_w=None, want_reps
         pair_audit_rule(B, nv, gmax, offsets, scores, rewards, p, pi_w, rule, wmax, seed, rep0, R,
                         out["mse"], out["bias_norm"], out["rep_sqerr"], out["edge_count"],
                         workspace, out["status"], stream)
+    return out
+
+
+def audit_exact(offsets, scores, rewards, p, gmax, pi_w=None, rule=RULE_HT, wmax=0.0,
+                want_gram=False, nv=None, workspace=None, stream=None):
+    """Exact design MSE and bias norm per prompt (no draws); optional Gram."""
+    B = offsets.numel() - 1
+    nv = _nv(offsets) if nv is None else nv
+    dev = scores.device
+    need = pair_audit_exact_workspace_bytes(B, gmax, scores.shape[1])
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    out = {
+        "mse": torch.empty(B, dtype=torch.float64, device=dev),
+        "bias_norm": torch.empty(B, dtype=torch.float64, device=dev),
+        "gram": torch.zeros((B, gmax, gmax), dtype=torch.float64, device=dev) if want_gram else None,
+        "status": torch.zeros(1, dtype=torch.int32, device=dev),
+    }
+    pair_audit_exact(B, nv, gmax, offsets, scores, rewards, p, pi_w, rule, wmax, out["mse"],
+                     out["bias_norm"], out["gram"], workspace, out["status"], stream)
     return out

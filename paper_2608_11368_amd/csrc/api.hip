@@ -145,6 +145,36 @@ int pair_audit_rule(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                             as_stream(stream));
 }
 
+size_t pair_audit_exact_workspace_bytes(int64_t B, int32_t gmax, int64_t D) {
+  if (B < 1 || gmax < 2 || gmax > PAIR_GMAX_LIMIT || D < 1 || D > kMaxCount) return 0;
+  return pair::exact_workspace_bytes(B, gmax, D);
+}
+
+int pair_audit_exact(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                     const void* scores, int32_t dtype, int64_t ld, const float* rewards,
+                     const float* p, const float* pi_w, int32_t rule, float wmax, double* mse,
+                     double* bias_norm, double* gram, void* workspace, size_t ws_bytes,
+                     int32_t* d_status, void* stream) {
+  int st = check_groups(B, nv, gmax, offsets);
+  if (st) return st;
+  st = check_rule(rule, wmax);
+  if (st) return st;
+  if (rule == PAIR_RULE_RATIO_KE || rule == PAIR_RULE_SELFNORM) return PAIR_EINVAL;
+  if (dtype != PAIR_BF16) return PAIR_EDTYPE;
+  st = check_scores(scores, dtype, D, ld);
+  if (st) return st;
+  if (rewards == nullptr || p == nullptr || mse == nullptr || bias_norm == nullptr)
+    return PAIR_EINVAL;
+  const size_t need = pair_audit_exact_workspace_bytes(B, gmax, D);
+  if (need == 0) return PAIR_ERANGE;
+  if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 ||
+      ws_bytes < need)
+    return PAIR_EWORKSPACE;
+  return pair::launch_audit_exact(B, nv, gmax, offsets, D, scores, ld, rewards, p, pi_w, rule,
+                                  wmax, mse, bias_norm, gram, workspace, d_status,
+                                  as_stream(stream));
+}
+
 int pair_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
                const void* scores, int32_t dtype, int64_t ld, const float* rewards,
                const float* p, const float* pi_w, uint64_t seed, int64_t rep0, int64_t R,

@@ -33,4 +33,12 @@ int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, in
                  double* bias_norm, float* rep_sqerr, int32_t* edge_count, void* workspace,
                  int32_t* d_status, hipStream_t stream);
 
+size_t exact_workspace_bytes(int64_t B, int32_t gmax, int64_t D);
+
+int launch_audit_exact(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                       const void* scores, int64_t ld, const float* rewards, const float* p,
+                       const float* pi_w, int32_t rule, float wmax, double* mse,
+                       double* bias_norm, double* gram, void* workspace, int32_t* d_status,
+                       hipStream_t stream);
+
 }  // namespace pair
