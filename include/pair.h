@@ -60,6 +60,9 @@ extern "C" {
 #define PAIR_ST_RHO_RANGE 2  /* an OBSERVED edge has rho outside (0, 1]        */
 #define PAIR_ST_P_RANGE 4    /* a continuation probability outside (0, 1]      */
 #define PAIR_ST_NONFINITE 8  /* a non-finite score in an audited score block    */
+#define PAIR_ST_BUDGET 16    /* design: budget below pi_min * sum(c), or an
+                                invalid prefix statistic (p outside [0, 1],
+                                c or m not positive and finite)               */
 
 /* Edge-weight rules: the estimator variants compared in the paper's audit and
  * ablation tables (Sec. 5, Tables 2, 4, 5; App. A "Naive selection bias" and
@@ -83,6 +86,11 @@ extern "C" {
 #define PAIR_RULE_CLIPPED 3
 #define PAIR_RULE_SELFNORM 4
 #define PAIR_RULE_MARGINAL 5
+
+/* Probability designs for pair_design_alloc. */
+#define PAIR_DESIGN_PAIR 0       /* graph-coupled convex design, Sec. 3.4        */
+#define PAIR_DESIGN_POINTWISE 1  /* pointwise p (1 - p) allocation               */
+#define PAIR_DESIGN_UNIFORM 2    /* one probability, the same expected cost      */
 
 /* Largest group size supported by the design draw, the coefficient fold and
  * the audit (one 64-lane wavefront holds one prompt's vertices). */
@@ -117,6 +125,42 @@ int pair_design_inclusion(int64_t B, int64_t nv, int32_t gmax, const int64_t* of
                           const float* p, uint64_t seed, int64_t rep0, int64_t R,
                           uint8_t* mask, float* pi, int32_t* edge_count, int32_t* completed,
                           int32_t* d_status, void* stream);
+
+/*
+ * pair_design_alloc -- graph-coupled probability design (paper Sec. 3.3 and
+ * Sec. 3.4, Eqs. (disagreement), (edge-proxy), (convex-objective), (budget)):
+ * continuation probabilities for every prompt from its prefix statistics.
+ *     d_ij = p_i (1 - p_j) + (1 - p_i) p_j,  a_ij = d_ij [ (m_i + m_j)^2 / 4 ]
+ *     b_i  = (sum_{j != i} sqrt(a_ij))^2 - sum_{j != i} a_ij
+ *     pi = argmin sum_{i<j} a_ij / (pi_i pi_j) + sum_i b_i / pi_i
+ *          s.t. sum_i c_i pi_i <= budget_b,  pi_min <= pi_i <= 1
+ * (the paper's program in pi_i = e^{-x_i}), solved to the optimum in fp64:
+ * exact cyclic coordinate minimisation of the Lagrangian for a multiplier
+ * found by bisection.  The budget is spent exactly unless sum_i c_i <=
+ * budget_b (then pi = 1).  Vertices with no contrast to any other vertex
+ * (all a_ij = 0 and b_i = 0) take pi_min.  The PAIR_DESIGN_POINTWISE design
+ * is the same program with a = 0 and b_i = p_i (1 - p_i); PAIR_DESIGN_UNIFORM
+ * is pi_i = clip(budget_b / sum_i c_i, pi_min, 1).  The output feeds
+ * pair_design_inclusion as p.
+ *
+ *   p_hat          fp32 [nv] predicted success probabilities in [0, 1]
+ *   c_hat          fp32 [nv] predicted remaining costs (> 0)
+ *   m_hat          fp32 [nv] score-norm predictions (>= 0) for the scaled
+ *                  proxy, or NULL for the parameter-free a = d
+ *   budget         fp32 [B] expected-cost budget of each prompt (> 0)
+ *   pi_min         probability floor in (0, 1] (the paper's default: 0.08)
+ *   design         PAIR_DESIGN_*
+ *   pi             fp32 [nv] out: continuation probabilities
+ *   objective      fp64 [B] out: the PAIR proxy Phi at pi (every design)  (or NULL)
+ *   iters          int32 [B] out: coordinate sweeps used                  (or NULL)
+ * Group sizes 1 <= G_b <= gmax <= 64.  Device status: PAIR_ST_BAD_GROUP;
+ * PAIR_ST_BUDGET (budget_b < pi_min sum c: that prompt gets pi = pi_min;
+ * invalid statistics: pi = pi_min).
+ */
+int pair_design_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                      const float* p_hat, const float* c_hat, const float* m_hat,
+                      const float* budget, float pi_min, int32_t design, float* pi,
+                      double* objective, int32_t* iters, int32_t* d_status, void* stream);
 
 /*
  * pair_edge_coeffs -- pair-corrected sequence advantages, paper Eq.

@@ -29,6 +29,10 @@ ST_BAD_GROUP = 1
 ST_RHO_RANGE = 2
 ST_P_RANGE = 4
 ST_NONFINITE = 8
+ST_BUDGET = 16
+DESIGN_PAIR = 0
+DESIGN_POINTWISE = 1
+DESIGN_UNIFORM = 2
 GMAX_LIMIT = 64
 
 RULE_HT = 0
@@ -38,7 +42,7 @@ RULE_CLIPPED = 3
 RULE_SELFNORM = 4
 RULE_MARGINAL = 5
 
-EXPORTED = ("pair_design_inclusion", "pair_edge_coeffs", "pair_edge_coeffs_rule",
+EXPORTED = ("pair_design_alloc", "pair_design_inclusion", "pair_edge_coeffs", "pair_edge_coeffs_rule",
             "pair_weighted_grad", "pair_audit_workspace_bytes", "pair_audit", "pair_audit_rule",
             "pair_audit_exact_workspace_bytes", "pair_audit_exact", "pair_strerror",
             "pair_version")
@@ -78,6 +82,8 @@ def lib() -> ctypes.CDLL:
         L.pair_audit_exact.argtypes = [i64, i64, i32, P, i64, P, i32, i64, P, P, P, i32, f32, P, P,
                                        P, P, ctypes.c_size_t, P, P]
         L.pair_audit_exact.restype = ctypes.c_int
+        L.pair_design_alloc.argtypes = [i64, i64, i32, P, P, P, P, P, f32, i32, P, P, P, P, P]
+        L.pair_design_alloc.restype = ctypes.c_int
         L.pair_weighted_grad.argtypes = [i64, i64, P, i64, P, i32, i64, P, P, i32, P, P]
         L.pair_weighted_grad.restype = ctypes.c_int
         L.pair_audit_workspace_bytes.argtypes = [i64, i32, i64, i64]
@@ -153,6 +159,18 @@ def pair_design_inclusion(B, nv, gmax, offsets, p, seed, rep0, R, mask=None, pi=
         _dev(edge_count, "edge_count", torch.int32, R * B, True),
         _dev(completed, "completed", torch.int32, R * B, True),
         _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_design_inclusion")
+
+
+def pair_design_alloc(B, nv, gmax, offsets, p_hat, c_hat, m_hat, budget, pi_min, design, pi,
+                      objective=None, iters=None, d_status=None, stream=None):
+    _rc(lib().pair_design_alloc(
+        B, nv, gmax, _dev(offsets, "offsets", torch.int64, B + 1),
+        _dev(p_hat, "p_hat", torch.float32, nv), _dev(c_hat, "c_hat", torch.float32, nv),
+        _dev(m_hat, "m_hat", torch.float32, nv, True), _dev(budget, "budget", torch.float32, B),
+        float(pi_min), int(design), _dev(pi, "pi", torch.float32, nv),
+        _dev(objective, "objective", torch.float64, B, True),
+        _dev(iters, "iters", torch.int32, B, True),
+        _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_design_alloc")
 
 
 def pair_edge_coeffs(B, nv, gmax, offsets, rewards, mask, pi, coeff, edge_count=None,
@@ -328,4 +346,22 @@ def audit_exact(offsets, scores, rewards, p, gmax, pi_w=None, rule=RULE_HT, wmax
     }
     pair_audit_exact(B, nv, gmax, offsets, scores, rewards, p, pi_w, rule, wmax, out["mse"],
                      out["bias_norm"], out["gram"], workspace, out["status"], stream)
+    return out
+
+
+def design_alloc(offsets, p_hat, c_hat, budget, gmax, pi_min=0.08, design=DESIGN_PAIR, m_hat=None,
+                 nv=None, stream=None):
+    """Continuation probabilities of every prompt (fp32 [nv]) with the
+    objective, sweep counts and status."""
+    B = offsets.numel() - 1
+    nv = _nv(offsets) if nv is None else nv
+    dev = p_hat.device
+    out = {
+        "pi": torch.empty(nv, dtype=torch.float32, device=dev),
+        "objective": torch.empty(B, dtype=torch.float64, device=dev),
+        "iters": torch.empty(B, dtype=torch.int32, device=dev),
+        "status": torch.zeros(1, dtype=torch.int32, device=dev),
+    }
+    pair_design_alloc(B, nv, gmax, offsets, p_hat, c_hat, m_hat, budget, pi_min, design, out["pi"],
+                      out["objective"], out["iters"], out["status"], stream)
     return out

@@ -145,6 +145,21 @@ int pair_audit_rule(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                             as_stream(stream));
 }
 
+int pair_design_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                      const float* p_hat, const float* c_hat, const float* m_hat,
+                      const float* budget, float pi_min, int32_t design, float* pi,
+                      double* objective, int32_t* iters, int32_t* d_status, void* stream) {
+  if (offsets == nullptr || p_hat == nullptr || c_hat == nullptr || budget == nullptr ||
+      pi == nullptr)
+    return PAIR_EINVAL;
+  if (B < 1 || B > 0x7fffffffLL || nv < 0 || nv > kMaxCount) return PAIR_EINVAL;
+  if (gmax < 1 || gmax > PAIR_GMAX_LIMIT) return PAIR_ERANGE;
+  if (design < PAIR_DESIGN_PAIR || design > PAIR_DESIGN_UNIFORM) return PAIR_EINVAL;
+  if (!(pi_min > 0.0f && pi_min <= 1.0f)) return PAIR_ERANGE;
+  return pair::launch_alloc(B, nv, gmax, offsets, p_hat, c_hat, m_hat, budget, pi_min, design, pi,
+                            objective, iters, d_status, as_stream(stream));
+}
+
 size_t pair_audit_exact_workspace_bytes(int64_t B, int32_t gmax, int64_t D) {
   if (B < 1 || gmax < 2 || gmax > PAIR_GMAX_LIMIT || D < 1 || D > kMaxCount) return 0;
   return pair::exact_workspace_bytes(B, gmax, D);

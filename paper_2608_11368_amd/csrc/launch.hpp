@@ -33,6 +33,11 @@ int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, in
                  double* bias_norm, float* rep_sqerr, int32_t* edge_count, void* workspace,
                  int32_t* d_status, hipStream_t stream);
 
+int launch_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, const float* p_hat,
+                 const float* c_hat, const float* m_hat, const float* budget, float pi_min,
+                 int32_t design, float* pi, double* objective, int32_t* iters, int32_t* d_status,
+                 hipStream_t stream);
+
 size_t exact_workspace_bytes(int64_t B, int32_t gmax, int64_t D);
 
 int launch_audit_exact(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,

@@ -155,6 +155,29 @@ def host_meta(w: Workload, seed: int | None = None) -> HostMeta:
     return HostMeta(offsets=offsets, rewards=rew, p=pr, gmax=int(w.gmax))
 
 
+@dataclasses.dataclass
+class AllocInputs:
+    p_hat: np.ndarray      # float32 [nv] predicted success probabilities
+    c_hat: np.ndarray      # float32 [nv] predicted remaining suffix tokens
+    budget: np.ndarray     # float32 [B] expected-cost budget per prompt
+
+
+def alloc_inputs(w: Workload, offsets: np.ndarray, ratio: float = 0.5,
+                 seed: int | None = None) -> AllocInputs:
+    """Prefix statistics for the probability design: predicted success
+    uniform on [0.02, 0.98], predicted suffix lengths LogNormal with mean 4000
+    tokens (sigma 1), and a budget of `ratio` times each prompt's total
+    predicted cost (the configuration's default budget ratio is 0.5)."""
+    rng = np.random.default_rng((w.data_seed if seed is None else seed) + 104729)
+    nv = int(offsets[-1])
+    p_hat = rng.uniform(0.02, 0.98, nv).astype(np.float32)
+    sigma = 1.0
+    c_hat = rng.lognormal(math.log(4000.0) - 0.5 * sigma * sigma, sigma, nv).astype(np.float32)
+    budget = np.array([ratio * float(np.sum(c_hat[offsets[b]:offsets[b + 1]], dtype=np.float64))
+                       for b in range(offsets.size - 1)], dtype=np.float32)
+    return AllocInputs(p_hat=p_hat, c_hat=c_hat, budget=budget)
+
+
 def score_scale(w: Workload) -> float:
     return 1.0 if w.score_std == "unit" else 1.0 / math.sqrt(w.D)
 
