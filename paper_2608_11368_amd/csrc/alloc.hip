@@ -15,10 +15,10 @@
 //     pi_i = clip( sqrt(A_i / (lam c_i)), pi_min, 1 ).
 // For a fixed multiplier lam, cyclic coordinate descent with these exact
 // updates converges to the minimiser of the (convex) Lagrangian; the spent
-// budget c^T pi(lam) does not increase with lam, so lam is found by
-// bisection in log space between a multiplier that puts every vertex at
-// pi_min and one that puts every vertex with positive A at 1, each inner
-// solve warm-started from the previous one.  A_i for one coordinate is a
+// budget c^T pi(lam) does not increase with lam, so lam is found by a
+// safeguarded false-position search (Illinois) in log space between a
+// multiplier that puts every vertex at pi_min and one that puts every vertex
+// with positive A at 1, each inner solve warm-started from the previous one.  A_i for one coordinate is a
 // wave reduction in which lane j contributes a_ji / pi_j, with a_ji formed on
 // the fly from p_j and the wave-uniform p_i, so nothing G x G is stored.
 //
@@ -34,12 +34,34 @@ namespace pair {
 namespace {
 
 constexpr int kMaxSweeps = 400;     // inner coordinate-descent sweeps per multiplier
-constexpr int kMaxBisect = 120;     // multiplier bisection steps
+constexpr int kMaxBisect = 200;     // multiplier search steps
 
+// 64-bit DPP move of a double (two 32-bit halves), all rows and banks on.
+template <int kCtrl>
+__device__ __forceinline__ double dpp_d(double v) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, kCtrl, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), kCtrl, 0xf, 0xf, false);
+  return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+__device__ __forceinline__ double readlane_d(double v, int lane) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), lane);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+// Wave sum in a fixed order, the same value in every lane: within each row of
+// 16 lanes, pairwise exchanges (quad_perm [1,0,3,2], quad_perm [2,3,0,1],
+// row_half_mirror, row_mirror) leave the row total in every lane of the row;
+// the four row totals are then added in row order.
 __device__ __forceinline__ double wave_sum_d(double v) {
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) v += __shfl_xor(v, m, kWave);
-  return v;
+  v += dpp_d<0xB1>(v);     // quad_perm [1,0,3,2]
+  v += dpp_d<0x4E>(v);     // quad_perm [2,3,0,1]
+  v += dpp_d<0x141>(v);    // row_half_mirror
+  v += dpp_d<0x140>(v);    // row_mirror
+  return ((readlane_d(v, 0) + readlane_d(v, 16)) + readlane_d(v, 32)) + readlane_d(v, 48);
 }
 
 __device__ __forceinline__ double wave_max_d(double v) {
@@ -91,7 +113,7 @@ __global__ __launch_bounds__(kWave) void alloc_kernel(
   // Vertex term b_i (pointwise design: p (1 - p)); A_i's range over the box.
   double bv = 0.0, arow = 0.0;
   for (int i = 0; i < gi; ++i) {
-    const double p_i = __shfl(p, i, kWave), m_i = __shfl(m, i, kWave);
+    const double p_i = readlane_d(p, i), m_i = readlane_d(m, i);
     const double a = (vert && lane != i && design == PAIR_DESIGN_PAIR)
                          ? proxy(p_i, p, m_i, m, scaled) : 0.0;
     const double s1 = wave_sum_d(sqrt(a)), s2 = wave_sum_d(a);
@@ -124,16 +146,18 @@ __global__ __launch_bounds__(kWave) void alloc_kernel(
     if (!(lam_hi > 0.0)) {
       pi = pmin;   // no contrast anywhere: the cheapest feasible design
     } else {
-      double llo = log(fmin(lam_lo, lam_hi * 0.5)), lhi = log(lam_hi);
-      pi = 1.0;
-      bool done = false;
-      for (int bis = 0; bis < kMaxBisect && !done; ++bis) {
-        const double lam = exp(0.5 * (llo + lhi));
-        // Inner cyclic coordinate descent at this multiplier.
+      // Root of f(t) = log(c^T pi(e^t)) - log(budget), nonincreasing in t,
+      // by Illinois false position on [tlo, thi]: f(tlo) >= 0 >= f(thi);
+      // when the same end is replaced twice in a row, the other end's value
+      // is halved.  Each evaluation is an inner coordinate descent at
+      // lam = e^t, warm-started from the previous iterate.
+      double spent = 0.0;
+      auto solve_at = [&](double t) -> double {
+        const double lam = exp(t);
         for (int sw = 0; sw < kMaxSweeps; ++sw) {
           double change = 0.0;
           for (int i = 0; i < gi; ++i) {
-            const double p_i = __shfl(p, i, kWave), m_i = __shfl(m, i, kWave);
+            const double p_i = readlane_d(p, i), m_i = readlane_d(m, i);
             const double a = (vert && lane != i && design == PAIR_DESIGN_PAIR)
                                  ? proxy(p_i, p, m_i, m, scaled) : 0.0;
             const double Ai = wave_sum_d(a / pi);
@@ -148,14 +172,38 @@ __global__ __launch_bounds__(kWave) void alloc_kernel(
           ++it;
           if (wave_max_d(change) <= 1e-13) break;
         }
-        const double spent = wave_sum_d(vert ? c * pi : 0.0);
-        if (fabs(spent - bud) <= 1e-13 * bud) done = true;
-        if (spent > bud) llo = log(lam); else lhi = log(lam);
-        if (lhi - llo <= 1e-15) done = true;
+        spent = wave_sum_d(vert ? c * pi : 0.0);
+        return log(spent) - log(bud);
+      };
+      double tlo = log(fmin(lam_lo, lam_hi * 0.5)), thi = log(lam_hi);
+      pi = 1.0;
+      double flo = solve_at(tlo);
+      if (flo > 0.0 && fabs(spent - bud) > 1e-13 * bud) {   // otherwise the budget does not bind
+        pi = pmin;
+        double fhi = solve_at(thi);
+        int side = 0;
+        for (int k = 0; k < kMaxBisect && fhi < 0.0 && fabs(spent - bud) > 1e-13 * bud; ++k) {
+          double t = (tlo * fhi - thi * flo) / (fhi - flo);
+          if (!(t > tlo && t < thi)) t = 0.5 * (tlo + thi);
+          const double ft = solve_at(t);
+          if (fabs(spent - bud) <= 1e-13 * bud) break;
+          if (ft > 0.0) {
+            tlo = t;
+            flo = ft;
+            if (side == 1) fhi *= 0.5;
+            side = 1;
+          } else {
+            thi = t;
+            fhi = ft;
+            if (side == -1) flo *= 0.5;
+            side = -1;
+          }
+          if (thi - tlo <= 1e-15) break;
+        }
       }
       // The last multiplier may leave the budget overspent by a rounding
       // amount: keep the iterate of the feasible side.
-      const double spent = wave_sum_d(vert ? c * pi : 0.0);
+      spent = wave_sum_d(vert ? c * pi : 0.0);
       if (spent > bud) pi = fmax(pmin, pi * (bud / spent));
     }
   }
@@ -165,15 +213,15 @@ __global__ __launch_bounds__(kWave) void alloc_kernel(
     // Phi at the returned probabilities (the PAIR proxy for every design).
     double phi = 0.0;
     for (int i = 0; i < gi; ++i) {
-      const double p_i = __shfl(p, i, kWave), m_i = __shfl(m, i, kWave);
-      const double pi_i = __shfl(pi, i, kWave);
+      const double p_i = readlane_d(p, i), m_i = readlane_d(m, i);
+      const double pi_i = readlane_d(pi, i);
       const double a = (vert && lane > i) ? proxy(p_i, p, m_i, m, scaled) : 0.0;
       phi += a / (pi_i * pi);
     }
     // b of the PAIR proxy (for the non-PAIR designs bv holds their own term).
     double bp = 0.0;
     for (int i = 0; i < gi; ++i) {
-      const double p_i = __shfl(p, i, kWave), m_i = __shfl(m, i, kWave);
+      const double p_i = readlane_d(p, i), m_i = readlane_d(m, i);
       const double a = (vert && lane != i) ? proxy(p_i, p, m_i, m, scaled) : 0.0;
       const double s1 = wave_sum_d(sqrt(a)), s2 = wave_sum_d(a);
       if (lane == i) bp = fmax(s1 * s1 - s2, 0.0);
