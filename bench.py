@@ -200,6 +200,46 @@ def cpu_baseline(meta, w, scores_dev, meta_a, wa, scores_a_dev, budget_s=12.0):
 RULE_NAMES = ("ht", "unweighted", "ratio_ke", "clipped", "selfnorm", "marginal")
 
 
+def time_alloc(pair, stream, wl, dev, reps=5):
+    """Probability design (Sec. 3.4) on the ragged workload's prompt structure
+    (B = 512, G_b ~ U{2..64}) with synthetic prefix statistics; each design
+    timed with events on the launch stream."""
+    import torch
+
+    w = wl.WORKLOADS["ragged"]
+    meta = wl.host_meta(w)
+    inp = wl.alloc_inputs(w, meta.offsets)
+    t = lambda a: torch.from_numpy(a).to(dev)
+    off, ph, ch, bu = t(meta.offsets), t(inp.p_hat), t(inp.c_hat), t(inp.budget)
+    B, nv = meta.B, meta.nv
+    pi = torch.empty(nv, dtype=torch.float32, device=dev)
+    obj = torch.empty(B, dtype=torch.float64, device=dev)
+    its = torch.empty(B, dtype=torch.int32, device=dev)
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+    out = {"workload": f"B={B}, G_b~U{{2..64}}, nv={nv}, budget 0.5 sum c, pi_min 0.08"}
+    with torch.cuda.stream(stream):
+        for name, design in (("pair", 0), ("pointwise", 1), ("uniform", 2)):
+            def run():
+                pair.pair_design_alloc(B, nv, meta.gmax, off, ph, ch, None, bu, 0.08, design, pi,
+                                       obj, its, st, stream)
+            run()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                run()
+            e1.record(stream)
+            e1.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            out[name] = {"ms": round(ms, 4), "prompts_per_s": round(B / (ms * 1e-3), 1),
+                         "mean_objective": float(obj.mean().item()),
+                         "sweeps_mean": round(float(its.float().mean().item()), 1),
+                         "sweeps_max": int(its.max().item())}
+    if int(st.item()) != 0:
+        raise RuntimeError(f"device status {int(st.item())} in the probability design")
+    return out
+
+
 def time_exact_audit(pair, stream, B, nv, G, off, scores, rew, p, D, reps=10):
     """Exact design audit (Gram on the matrix cores + closed form) on the
     audit workload, timed with events on the launch stream.  HBM-bound: the
@@ -463,6 +503,7 @@ def main():
     }
     result["exact_audit"] = time_exact_audit(pair, stream, Ba, nva, Ga, off_a, scores_a, rew_a,
                                              p_a, Da)
+    result["design_alloc"] = time_alloc(pair, stream, wl, dev)
     result["variants"] = time_variants(pair, stream, B, nv, G, off, rew, mask, pi, coeff,
                                        (Ba, nva, Ga, off_a, scores_a, rew_a, p_a, wa, R, mse, bias,
                                         reps, ec_a, ws), status)
