@@ -22,6 +22,11 @@ Parity status of each function (what pins it, see ``tests/test_oracle_pins.py``)
                     of the mean for every linear rule; zero bias for HT
                     (Thm 2); Prop. 1's unweighted bias vector; zero error
                     when p == 1
+  cps_*             conditional Poisson (fixed-size) design: inclusion
+                    probabilities pinned by brute force over every sample;
+                    the sequential draw's sample probabilities pinned to
+                    prod w / e_n by walking every path; the fit's output
+                    reproduces its target; draw frequencies vs pi and pi_ij
   *_rule variants   pinned by exhaustive design enumeration against the
                     expectations the paper states for each edge-weight rule
                     (naive bias, clipped multiplier min(1, w_max rho) - 1,
@@ -115,6 +120,12 @@ def _load():
         lib.orc_audit_exact.argtypes = [i64, P, i32, i64, P, ctypes.c_int, i64, P, P, P,
                                         ctypes.c_int, dbl, P, P]
         lib.orc_audit_exact.restype = ctypes.c_int
+        lib.orc_cps_inclusion.argtypes = [P, i64, i64, P, P]
+        lib.orc_cps_inclusion.restype = ctypes.c_int
+        lib.orc_cps_fit.argtypes = [P, i64, i64, dbl, i64, P, P]
+        lib.orc_cps_fit.restype = ctypes.c_int
+        lib.orc_cps_draw.argtypes = [i64, P, P, P, u64, i64, i64, P]
+        lib.orc_cps_draw.restype = ctypes.c_int
         lib.orc_num_threads.argtypes = []
         lib.orc_num_threads.restype = ctypes.c_int
         _lib = lib
@@ -319,3 +330,39 @@ def audit_exact(offsets, scores, rewards, p, pi_w=None, gmax=None, rule=RULE_HT,
     _check(lib.orc_audit_exact(B, _ptr(off), gmax, D, _ptr(s), code, ld, _ptr(r), _ptr(pp),
                                _ptr(pi_w), int(rule), float(wmax), _ptr(mse), _ptr(bias)))
     return {"mse": mse, "bias_norm": bias}
+
+
+def cps_inclusion(w, n):
+    """Conditional Poisson design of one prompt with odds w and size n:
+    returns (pi[g], pij[g][g]) in fp64 (pij's diagonal = pi)."""
+    lib = _load()
+    w = np.ascontiguousarray(w, dtype=np.float64)
+    g = w.size
+    pi = np.zeros(g)
+    pij = np.zeros((g, g))
+    _check(lib.orc_cps_inclusion(_ptr(w), g, int(n), _ptr(pi), _ptr(pij)))
+    return pi, pij
+
+
+def cps_fit(pi_target, n, tol=1e-12, max_iter=10000):
+    """Odds whose conditional Poisson design has first-order probabilities
+    pi_target (summing to n).  Returns (w, iterations; negative if not
+    converged)."""
+    lib = _load()
+    t = np.ascontiguousarray(pi_target, dtype=np.float64)
+    w = np.zeros(t.size)
+    it = np.zeros(1, dtype=np.int64)
+    _check(lib.orc_cps_fit(_ptr(t), t.size, int(n), float(tol), int(max_iter), _ptr(w), _ptr(it)))
+    return w, int(it[0])
+
+
+def cps_draw(offsets, w, n, seed, rep0, R):
+    """Fixed-size draws mask[R][nv] for every prompt (prompt ids 0..B-1)."""
+    lib = _load()
+    off = _offsets(offsets)
+    B = off.size - 1
+    w = np.ascontiguousarray(w, dtype=np.float64)
+    nn = np.ascontiguousarray(n, dtype=np.int32)
+    mask = np.zeros((R, int(off[-1])), dtype=np.uint8)
+    _check(lib.orc_cps_draw(B, _ptr(off), _ptr(w), _ptr(nn), seed, rep0, R, _ptr(mask)))
+    return mask

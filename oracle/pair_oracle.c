@@ -31,6 +31,9 @@
  *     rules, below)
  *   - Prop. 1 and App. A "Design covariance": the exact design bias and
  *     covariance trace of a linear rule (orc_audit_exact)
+ *   - App. B "Fixed-size and exact-cost designs": conditional Poisson
+ *     sampling of a fixed number of endpoints (Hajek 1964) with its exact,
+ *     non-factorising joint inclusion probabilities (orc_cps_*)
  *
  * Random design draws.  The paper only requires fresh randomisation for the
  * continuation indicators.  This oracle fixes one counter-based generator, the
@@ -595,6 +598,180 @@ int orc_audit_exact(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D,
             err = s;
         }
         free(v); free(t); free(mu); free(own);
+    }
+    return err;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Conditional Poisson sampling (App. B; Hajek 1964; Chen, Dempster and Liu  */
+/* 1994): a sample S of exactly n of the G units with                        */
+/*     P(S) = prod_{i in S} w_i / e_n(w),                                    */
+/* e_k the elementary symmetric polynomial of the odds w.  Then              */
+/*     pi_i  = w_i e_{n-1}(w without i) / e_n(w),                            */
+/*     pi_ij = w_i w_j e_{n-2}(w without i, j) / e_n(w).                     */
+/* Every polynomial is built by the textbook recursion over units,           */
+/* e_k(w_1..w_m) = e_k(w_1..w_{m-1}) + w_m e_{k-1}(w_1..w_{m-1}), all terms  */
+/* positive.                                                                 */
+/* ------------------------------------------------------------------------ */
+/* e_0..e_n of the units 0..g-1 except skip1 and skip2 (-1: none). */
+static void esp_excluding(const double* w, int64_t g, int64_t n, int64_t skip1, int64_t skip2,
+                          double* e) {
+    e[0] = 1.0;
+    for (int64_t k = 1; k <= n; ++k) e[k] = 0.0;
+    for (int64_t m = 0; m < g; ++m) {
+        if (m == skip1 || m == skip2) continue;
+        for (int64_t k = n; k >= 1; --k) e[k] = e[k] + w[m] * e[k - 1];
+    }
+}
+
+/* First- and second-order inclusion probabilities of one prompt's design:
+ * pi[i], pij[i * g + j] (pij[i * g + i] = pi[i]).  0 < n < g. */
+int orc_cps_inclusion(const double* w, int64_t g, int64_t n, double* pi, double* pij) {
+    if (g < 1 || n < 0 || n > g || w == NULL || pi == NULL) return ORC_EINVAL;
+    for (int64_t i = 0; i < g; ++i)
+        if (!(w[i] > 0.0 && w[i] < INFINITY)) return ORC_EINVAL;
+    double* e = (double*)malloc((size_t)(n + 1) * sizeof(double));
+    if (!e) return ORC_EINVAL;
+    esp_excluding(w, g, n, -1, -1, e);
+    const double en = e[n];
+    for (int64_t i = 0; i < g; ++i) {
+        if (n == 0) {
+            pi[i] = 0.0;
+            continue;
+        }
+        esp_excluding(w, g, n - 1, i, -1, e);
+        pi[i] = w[i] * e[n - 1] / en;
+    }
+    if (pij) {
+        for (int64_t i = 0; i < g; ++i) {
+            pij[i * g + i] = pi[i];
+            for (int64_t j = i + 1; j < g; ++j) {
+                double v = 0.0;
+                if (n >= 2) {
+                    esp_excluding(w, g, n - 2, i, j, e);
+                    v = w[i] * w[j] * e[n - 2] / en;
+                }
+                pij[i * g + j] = v;
+                pij[j * g + i] = v;
+            }
+        }
+    }
+    free(e);
+    return ORC_OK;
+}
+
+/* Odds w whose design has first-order probabilities pi_target (each in
+ * (0, 1), summing to the integer n within 1e-4 n; the target is first scaled
+ * by n / sum so that it sums to n): the fixed-point iteration
+ * w_i <- w_i pi_target_i / pi_i(w), rescaled to a geometric mean of 1 (the
+ * design does not change when every odds is multiplied by one constant),
+ * until max_i |pi_i(w) / pi_target_i - 1| <= tol or max_iter iterations.
+ * Returns the number of iterations in *iters (negative: not converged). */
+int orc_cps_fit(const double* pi_target, int64_t g, int64_t n, double tol, int64_t max_iter,
+                double* w, int64_t* iters) {
+    if (g < 1 || n < 1 || n >= g || pi_target == NULL || w == NULL) return ORC_EINVAL;
+    double sum = 0.0;
+    for (int64_t i = 0; i < g; ++i) {
+        if (!(pi_target[i] > 0.0 && pi_target[i] < 1.0)) return ORC_EP;
+        sum += pi_target[i];
+    }
+    if (fabs(sum - (double)n) > 1e-4 * (double)n) return ORC_EP;
+    double* pi = (double*)malloc((size_t)g * 2 * sizeof(double));
+    if (!pi) return ORC_EINVAL;
+    double* tg = pi + g;
+    for (int64_t i = 0; i < g; ++i) {
+        tg[i] = pi_target[i] * ((double)n / sum);
+        if (!(tg[i] < 1.0)) {
+            free(pi);
+            return ORC_EP;
+        }
+        w[i] = tg[i] / (1.0 - tg[i]);
+    }
+    int64_t it = 0;
+    int ok = 0;
+    for (; it < max_iter; ++it) {
+        orc_cps_inclusion(w, g, n, pi, NULL);
+        double err = 0.0, lg = 0.0;
+        for (int64_t i = 0; i < g; ++i) {
+            double r = fabs(pi[i] / tg[i] - 1.0);
+            if (r > err) err = r;
+        }
+        if (err <= tol) {
+            ok = 1;
+            break;
+        }
+        for (int64_t i = 0; i < g; ++i) {
+            w[i] *= tg[i] / pi[i];
+            lg += log(w[i]);
+        }
+        lg = exp(-lg / (double)g);
+        for (int64_t i = 0; i < g; ++i) w[i] *= lg;
+    }
+    free(pi);
+    if (iters) *iters = ok ? it : -it;
+    return ORC_OK;
+}
+
+/* Sequential conditional Poisson draw of one prompt for replicate r: units in
+ * order i = 0..g-1, with k units still to select, unit i is selected with
+ * probability w_i e_{k-1}(w_{i+1..g-1}) / e_k(w_{i..g-1}) (so the sample has
+ * exactly n units and probability prod w / e_n).  The uniform of unit i is
+ * the top 32 bits of Philox4x64-10 word (i & 3) at counter
+ * (r, prompt id, i >> 2, 0), key (seed, 0) -- the same reading as the
+ * Bernoulli draw -- and the unit is selected iff u_i < P * 2^32, all in fp64
+ * with unfused operations in the order written. */
+int orc_cps_draw_one(const double* w, int64_t g, int64_t n, uint64_t seed, int64_t r, int64_t bid,
+                     uint8_t* mask) {
+    if (g < 1 || n < 0 || n > g) return ORC_EINVAL;
+    /* suffix table E[i][k] = e_k(w_i .. w_{g-1}), i = g..0 */
+    double* E = (double*)calloc((size_t)(g + 1) * (size_t)(n + 1), sizeof(double));
+    if (!E) return ORC_EINVAL;
+    E[g * (n + 1) + 0] = 1.0;
+    for (int64_t i = g - 1; i >= 0; --i) {
+        E[i * (n + 1) + 0] = 1.0;
+        for (int64_t k = 1; k <= n; ++k) {
+            double t = w[i] * E[(i + 1) * (n + 1) + k - 1];
+            E[i * (n + 1) + k] = E[(i + 1) * (n + 1) + k] + t;
+        }
+    }
+    int64_t k = n;
+    uint64_t key[2] = {seed, 0};
+    for (int64_t i = 0; i < g; ++i) {
+        uint64_t ctr[4] = {(uint64_t)r, (uint64_t)bid, (uint64_t)(i >> 2), 0};
+        uint64_t out[4];
+        orc_philox4x64_10(ctr, key, out);
+        double u = (double)(out[i & 3] >> 32);
+        int take = 0;
+        if (k > 0) {
+            double num = w[i] * E[(i + 1) * (n + 1) + k - 1];
+            double prob = num / E[i * (n + 1) + k];
+            take = u < prob * 4294967296.0;
+        }
+        mask[i] = (uint8_t)take;
+        k -= take;
+    }
+    free(E);
+    return k == 0 ? ORC_OK : ORC_EINVAL;
+}
+
+/* Batched draw: mask[r][v] for replicates rep0..rep0+R-1 of every prompt,
+ * with per-prompt sizes n[b] and odds w[v]; prompt ids 0..B-1. */
+int orc_cps_draw(int64_t B, const int64_t* offsets, const double* w, const int32_t* n,
+                 uint64_t seed, int64_t rep0, int64_t R, uint8_t* mask) {
+    if (B < 1 || offsets == NULL || w == NULL || n == NULL || mask == NULL || R < 0)
+        return ORC_EINVAL;
+    int64_t nv = offsets[B];
+    int err = ORC_OK;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < R; ++r) {
+        for (int64_t b = 0; b < B; ++b) {
+            int64_t o = offsets[b], g = offsets[b + 1] - offsets[b];
+            int s = orc_cps_draw_one(w + o, g, n[b], seed, rep0 + r, b, mask + r * nv + o);
+            if (s) {
+#pragma omp critical
+                err = s;
+            }
+        }
     }
     return err;
 }
