@@ -163,6 +163,55 @@ int pair_design_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offset
                       double* objective, int32_t* iters, int32_t* d_status, void* stream);
 
 /*
+ * pair_cps_fit -- fixed-size continuation design (paper App. B "Fixed-size
+ * and exact-cost designs": conditional Poisson sampling, Hajek 1964): exactly
+ * n_b = round(sum_i pi_target_i) of the G_b candidates continue, each with
+ * first-order probability pi_target_i (the target is scaled by n_b / sum to
+ * sum to n_b exactly).  Samples S of size n_b have probability
+ * prod_{i in S} w_i / e_n(w) with odds w fitted here in fp64 (multiplicative
+ * fixed point w_i <- w_i pi_target_i / pi_i(w), to 1e-12 relative), and the
+ * exact joint probabilities
+ *     pi_ij = w_i w_j e_{n-2}(w without i, j) / e_n(w)
+ * do not factorise; they are what the estimator must weight with.
+ *
+ *   pi_target      fp32 [nv] in (0, 1), each prompt's sum within 1e-4 of an
+ *                  integer n_b with 1 <= n_b < G_b
+ *   w              fp64 [nv] out: the odds (geometric mean 1 per prompt)
+ *   n_out          int32 [B] out: n_b                                  (or NULL)
+ *   pi_joint       fp32 [B][gmax][gmax] out: pi_ij for i != j < G_b, pi_i on the
+ *                  diagonal, 0 beyond G_b -- the pi block that
+ *                  pair_edge_coeffs and pair_audit_rule take       (or NULL)
+ *   iters          int32 [B] out: fixed-point iterations (negative: not
+ *                  converged in 4000)                               (or NULL)
+ * Device status: PAIR_ST_BAD_GROUP; PAIR_ST_P_RANGE (a target outside (0, 1),
+ * a sum not within 1e-4 of an admissible integer, or no convergence: that
+ * prompt's w is 0 and n_b = 0).
+ */
+int pair_cps_fit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                 const float* pi_target, double* w, int32_t* n_out, float* pi_joint,
+                 int32_t* iters, int32_t* d_status, void* stream);
+
+/*
+ * pair_cps_draw -- fixed-size draws of the conditional Poisson design for
+ * replicates rep0 .. rep0+R-1: units are visited in order and unit i is
+ * selected with probability w_i e_{k-1}(w_{i+1..}) / e_k(w_{i..}), k the
+ * units still to select, so every draw has exactly n_b units and sample
+ * probability prod w / e_n.  The uniform for unit i is the top 32 bits of
+ * Philox4x64-10 word (i & 3) at counter (rep0 + r, b, i >> 2, 0), key
+ * (seed, 0), as in pair_design_inclusion; the threshold is computed in fp64
+ * with unfused operations in a fixed order.
+ *
+ *   w, n           from pair_cps_fit (w > 0 finite; 0 <= n_b <= G_b)
+ *   mask           uint8 [R][nv] out
+ *   edge_count     int32 [R][B] out: n_b (n_b - 1) / 2                  (or NULL)
+ * Device status: PAIR_ST_BAD_GROUP, PAIR_ST_P_RANGE (invalid w or n_b: that
+ * prompt's masks are not written).
+ */
+int pair_cps_draw(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, const double* w,
+                  const int32_t* n, uint64_t seed, int64_t rep0, int64_t R, uint8_t* mask,
+                  int32_t* edge_count, int32_t* d_status, void* stream);
+
+/*
  * pair_edge_coeffs -- pair-corrected sequence advantages, paper Eq.
  * (pair-advantage) with the enumeration of Algorithm 1 ("accumulate
  * h_ij / rho_ij into A~_i, A~_j") and App. C's numerics (fp32 accumulation,

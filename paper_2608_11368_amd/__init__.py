@@ -42,7 +42,7 @@ RULE_CLIPPED = 3
 RULE_SELFNORM = 4
 RULE_MARGINAL = 5
 
-EXPORTED = ("pair_design_alloc", "pair_design_inclusion", "pair_edge_coeffs", "pair_edge_coeffs_rule",
+EXPORTED = ("pair_design_alloc", "pair_cps_fit", "pair_cps_draw", "pair_design_inclusion", "pair_edge_coeffs", "pair_edge_coeffs_rule",
             "pair_weighted_grad", "pair_audit_workspace_bytes", "pair_audit", "pair_audit_rule",
             "pair_audit_exact_workspace_bytes", "pair_audit_exact", "pair_strerror",
             "pair_version")
@@ -84,6 +84,10 @@ def lib() -> ctypes.CDLL:
         L.pair_audit_exact.restype = ctypes.c_int
         L.pair_design_alloc.argtypes = [i64, i64, i32, P, P, P, P, P, f32, i32, P, P, P, P, P]
         L.pair_design_alloc.restype = ctypes.c_int
+        L.pair_cps_fit.argtypes = [i64, i64, i32, P, P, P, P, P, P, P, P]
+        L.pair_cps_fit.restype = ctypes.c_int
+        L.pair_cps_draw.argtypes = [i64, i64, i32, P, P, P, u64, i64, i64, P, P, P, P]
+        L.pair_cps_draw.restype = ctypes.c_int
         L.pair_weighted_grad.argtypes = [i64, i64, P, i64, P, i32, i64, P, P, i32, P, P]
         L.pair_weighted_grad.restype = ctypes.c_int
         L.pair_audit_workspace_bytes.argtypes = [i64, i32, i64, i64]
@@ -171,6 +175,27 @@ def pair_design_alloc(B, nv, gmax, offsets, p_hat, c_hat, m_hat, budget, pi_min,
         _dev(objective, "objective", torch.float64, B, True),
         _dev(iters, "iters", torch.int32, B, True),
         _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_design_alloc")
+
+
+def pair_cps_fit(B, nv, gmax, offsets, pi_target, w, n_out=None, pi_joint=None, iters=None,
+                 d_status=None, stream=None):
+    _rc(lib().pair_cps_fit(
+        B, nv, gmax, _dev(offsets, "offsets", torch.int64, B + 1),
+        _dev(pi_target, "pi_target", torch.float32, nv), _dev(w, "w", torch.float64, nv),
+        _dev(n_out, "n_out", torch.int32, B, True),
+        _dev(pi_joint, "pi_joint", torch.float32, B * gmax * gmax, True),
+        _dev(iters, "iters", torch.int32, B, True),
+        _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_cps_fit")
+
+
+def pair_cps_draw(B, nv, gmax, offsets, w, n, seed, rep0, R, mask, edge_count=None,
+                  d_status=None, stream=None):
+    _rc(lib().pair_cps_draw(
+        B, nv, gmax, _dev(offsets, "offsets", torch.int64, B + 1), _dev(w, "w", torch.float64, nv),
+        _dev(n, "n", torch.int32, B), ctypes.c_uint64(seed & ((1 << 64) - 1)), rep0, R,
+        _dev(mask, "mask", torch.uint8, R * nv),
+        _dev(edge_count, "edge_count", torch.int32, R * B, True),
+        _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_cps_draw")
 
 
 def pair_edge_coeffs(B, nv, gmax, offsets, rewards, mask, pi, coeff, edge_count=None,
@@ -364,4 +389,36 @@ def design_alloc(offsets, p_hat, c_hat, budget, gmax, pi_min=0.08, design=DESIGN
     }
     pair_design_alloc(B, nv, gmax, offsets, p_hat, c_hat, m_hat, budget, pi_min, design, out["pi"],
                       out["objective"], out["iters"], out["status"], stream)
+    return out
+
+
+def cps_fit(offsets, pi_target, gmax, nv=None, stream=None):
+    """Fixed-size design from target probabilities: dict(w, n, pi_joint, iters, status)."""
+    B = offsets.numel() - 1
+    nv = _nv(offsets) if nv is None else nv
+    dev = pi_target.device
+    out = {
+        "w": torch.empty(nv, dtype=torch.float64, device=dev),
+        "n": torch.empty(B, dtype=torch.int32, device=dev),
+        "pi_joint": torch.empty((B, gmax, gmax), dtype=torch.float32, device=dev),
+        "iters": torch.empty(B, dtype=torch.int32, device=dev),
+        "status": torch.zeros(1, dtype=torch.int32, device=dev),
+    }
+    pair_cps_fit(B, nv, gmax, offsets, pi_target, out["w"], out["n"], out["pi_joint"],
+                 out["iters"], out["status"], stream)
+    return out
+
+
+def cps_draw(offsets, w, n, seed, rep0, R, gmax, nv=None, stream=None):
+    """Fixed-size draws: dict(mask[R][nv], edge_count[R][B], status)."""
+    B = offsets.numel() - 1
+    nv = _nv(offsets) if nv is None else nv
+    dev = w.device
+    out = {
+        "mask": torch.empty((R, nv), dtype=torch.uint8, device=dev),
+        "edge_count": torch.empty((R, B), dtype=torch.int32, device=dev),
+        "status": torch.zeros(1, dtype=torch.int32, device=dev),
+    }
+    pair_cps_draw(B, nv, gmax, offsets, w, n, seed, rep0, R, out["mask"], out["edge_count"],
+                  out["status"], stream)
     return out

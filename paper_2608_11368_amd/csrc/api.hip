@@ -160,6 +160,28 @@ int pair_design_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offset
                             objective, iters, d_status, as_stream(stream));
 }
 
+int pair_cps_fit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                 const float* pi_target, double* w, int32_t* n_out, float* pi_joint,
+                 int32_t* iters, int32_t* d_status, void* stream) {
+  int st = check_groups(B, nv, gmax, offsets);
+  if (st) return st;
+  if (pi_target == nullptr || w == nullptr) return PAIR_EINVAL;
+  return pair::launch_cps_fit(B, nv, gmax, offsets, pi_target, w, n_out, pi_joint, iters,
+                              d_status, as_stream(stream));
+}
+
+int pair_cps_draw(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, const double* w,
+                  const int32_t* n, uint64_t seed, int64_t rep0, int64_t R, uint8_t* mask,
+                  int32_t* edge_count, int32_t* d_status, void* stream) {
+  if (offsets == nullptr || w == nullptr || n == nullptr || mask == nullptr) return PAIR_EINVAL;
+  if (B < 1 || B > 0x7fffffffLL || nv < 0 || nv > kMaxCount) return PAIR_EINVAL;
+  if (gmax < 1 || gmax > PAIR_GMAX_LIMIT) return PAIR_ERANGE;
+  if (R < 1 || rep0 < 0 || R > kMaxCount || rep0 > kMaxCount || R > kMaxCount / (nv > 0 ? nv : 1))
+    return PAIR_ERANGE;
+  return pair::launch_cps_draw(B, nv, gmax, offsets, w, n, seed, rep0, R, mask, edge_count,
+                               d_status, as_stream(stream));
+}
+
 size_t pair_audit_exact_workspace_bytes(int64_t B, int32_t gmax, int64_t D) {
   if (B < 1 || gmax < 2 || gmax > PAIR_GMAX_LIMIT || D < 1 || D > kMaxCount) return 0;
   return pair::exact_workspace_bytes(B, gmax, D);

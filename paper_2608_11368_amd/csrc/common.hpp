@@ -130,6 +130,40 @@ __device__ __forceinline__ bool rule_term(int rule, float wmax, float dr, float 
   }
 }
 
+// 64-bit DPP move of a double (two 32-bit halves), all rows and banks on.
+template <int kCtrl>
+__device__ __forceinline__ double dpp_d(double v) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, kCtrl, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), kCtrl, 0xf, 0xf, false);
+  return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+__device__ __forceinline__ double readlane_d(double v, int lane) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), lane);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+// Wave sum in a fixed order, the same value in every lane: within each row of
+// 16 lanes, pairwise exchanges (quad_perm [1,0,3,2], quad_perm [2,3,0,1],
+// row_half_mirror, row_mirror) leave the row total in every lane of the row;
+// the four row totals are then added in row order.
+__device__ __forceinline__ double wave_sum_d(double v) {
+  v += dpp_d<0xB1>(v);     // quad_perm [1,0,3,2]
+  v += dpp_d<0x4E>(v);     // quad_perm [2,3,0,1]
+  v += dpp_d<0x141>(v);    // row_half_mirror
+  v += dpp_d<0x140>(v);    // row_mirror
+  return ((readlane_d(v, 0) + readlane_d(v, 16)) + readlane_d(v, 32)) + readlane_d(v, 48);
+}
+
+__device__ __forceinline__ double wave_max_d(double v) {
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) v = fmax(v, __shfl_xor(v, m, kWave));
+  return v;
+}
+
 // Validated bounds of prompt b: returns false (and sets the status bit) when
 // the offsets are not monotone, leave [0, nv], or G_b is outside [gmin, gmax].
 __device__ __forceinline__ bool prompt_bounds(const int64_t* offsets, int64_t b, int64_t nv,

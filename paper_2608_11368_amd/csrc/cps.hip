@@ -1,0 +1,267 @@
+// Conditional Poisson (fixed-size) design: paper App. B "Fixed-size and
+// exact-cost designs" (Hajek 1964 rejective sampling): exactly n of the G
+// candidates continue, with first-order probabilities prescribed by the
+// allocation and joint probabilities that do not factorise and are computed
+// exactly from the design.
+//
+// With odds w, P(S) = prod_{i in S} w_i / e_n(w) over |S| = n, where e_k is
+// the elementary symmetric polynomial, and
+//     pi_i  = w_i e_{n-1}(w without i) / e_n(w),
+//     pi_ij = w_i w_j e_{n-2}(w without i, j) / e_n(w)
+//           = (w_j pi_i - w_i pi_j) / (w_j - w_i)          (w_i != w_j).
+//
+//  cps_fit_kernel   one wavefront per prompt, lane i = unit i, fp64.  Each
+//                   lane keeps its leave-one-out polynomial e_k(w without i),
+//                   k <= n, in registers (the recursion over units adds
+//                   w_m e_{k-1} into e_k, with w_m = 0 for m = i, which adds
+//                   exactly nothing); the odds follow the multiplicative fixed
+//                   point w_i <- w_i pi_target_i / pi_i(w), renormalised to a
+//                   geometric mean of 1, until every pi_i is within 1e-12 of
+//                   its target.  The joint block uses the difference formula
+//                   when the two odds differ by more than 1% and the direct
+//                   leave-two-out polynomial otherwise.
+//  cps_draw_kernel  lane = replicate.  The workgroup builds the suffix table
+//                   E[i][k] = e_k(w_i .. w_{G-1}) in LDS (lane k, units from
+//                   the last); each lane then walks the units in order and
+//                   selects unit i with probability
+//                   w_i E[i+1][k-1] / E[i][k], k the units still to select,
+//                   comparing the top 32 bits of Philox4x64-10 word (i & 3) at
+//                   counter (replicate, prompt, i >> 2, 0) with that
+//                   probability times 2^32.  The table and the thresholds use
+//                   unfused fp64 operations in a fixed order, so each draw is
+//                   a deterministic function of (seed, replicate, prompt, w).
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace pair {
+
+namespace {
+
+constexpr int kMaxFitIter = 4000;
+
+// e_0..e_{KP-1} (only k <= n meaningful) of the units 0..g-1 excluding skip1
+// and skip2, the units' odds taken from the wave (lane m holds w_m).
+template <int KP>
+__device__ __forceinline__ void esp_excl(double w, int g, int n, int skip1, int skip2,
+                                         double (&e)[KP]) {
+  e[0] = 1.0;
+#pragma unroll
+  for (int k = 1; k < KP; ++k) e[k] = 0.0;
+  for (int m = 0; m < g; ++m) {
+    const double wm0 = readlane_d(w, m);
+    const double wm = (m == skip1 || m == skip2) ? 0.0 : wm0;
+#pragma unroll
+    for (int k = KP - 1; k >= 1; --k)
+      if (k <= n) e[k] = __dadd_rn(e[k], __dmul_rn(wm, e[k - 1]));
+  }
+}
+
+// e[k] for a run-time k, by an unrolled select (keeps e in registers).
+template <int KP>
+__device__ __forceinline__ double pick(const double (&e)[KP], int k) {
+  double v = 0.0;
+#pragma unroll
+  for (int q = 0; q < KP; ++q) v = q == k ? e[q] : v;
+  return v;
+}
+
+__device__ __forceinline__ uint64_t philox_word(const Philox4x64& x, int q) {
+  return q == 0 ? x.w[0] : (q == 1 ? x.w[1] : (q == 2 ? x.w[2] : x.w[3]));
+}
+
+template <int KP>
+__global__ __launch_bounds__(kWave) void cps_fit_kernel(
+    int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets,
+    const float* __restrict__ pi_target, double* __restrict__ w_out, int32_t* __restrict__ n_out,
+    float* __restrict__ pi_joint, int32_t* __restrict__ iters, int32_t* d_status) {
+  const int64_t b = blockIdx.x;
+  const int lane = threadIdx.x;
+  int64_t o0, g64;
+  if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g64, d_status, lane == 0)) return;
+  const int g = (int)g64;
+  const bool unit = lane < g;
+  double t = unit ? (double)pi_target[o0 + lane] : 0.0;
+  const double sum = wave_sum_d(t);
+  const int n = (int)rint(sum);
+  bool bad = unit && !(t > 0.0 && t < 1.0);
+  bad = __ballot(bad) != 0ull || n < 1 || n >= g || fabs(sum - (double)n) > 1e-4 * (double)n;
+  if (!bad) {
+    t = unit ? t * ((double)n / sum) : 0.0;
+    bad = __ballot(unit && !(t < 1.0)) != 0ull;
+  }
+  if (bad) {
+    if (lane == 0) {
+      raise_status(d_status, PAIR_ST_P_RANGE);
+      if (n_out != nullptr) n_out[b] = 0;
+      if (iters != nullptr) iters[b] = 0;
+    }
+    if (unit) w_out[o0 + lane] = 0.0;
+    return;
+  }
+
+  double w = unit ? t / (1.0 - t) : 0.0;
+  double e[KP];
+  int it = 0;
+  bool converged = false;
+  for (; it < kMaxFitIter; ++it) {
+    esp_excl<KP>(w, g, n, lane, -1, e);
+    double pi = 0.0;
+    if (unit) {
+      const double e1 = pick<KP>(e, n - 1);
+      const double en = pick<KP>(e, n) + w * e1;   // e_n(w) from the leave-one-out polynomial
+      pi = w * e1 / en;
+    }
+    const double err = wave_max_d(unit ? fabs(pi / t - 1.0) : 0.0);
+    if (err <= 1e-12) {
+      converged = true;
+      break;
+    }
+    if (unit) w *= t / pi;
+    const double lg = wave_sum_d(unit ? log(w) : 0.0) / (double)g;
+    w = unit ? w * exp(-lg) : 0.0;
+  }
+  if (!converged && lane == 0) raise_status(d_status, PAIR_ST_P_RANGE);
+  if (unit) w_out[o0 + lane] = w;
+  if (lane == 0) {
+    if (n_out != nullptr) n_out[b] = n;
+    if (iters != nullptr) iters[b] = converged ? it : -it;
+  }
+
+  if (pi_joint != nullptr) {
+    // pi_i of every unit (lane), then row i of the joint block by lane i.
+    esp_excl<KP>(w, g, n, lane, -1, e);
+    double pi = 0.0, en = 1.0;
+    if (unit) {
+      const double e1 = pick<KP>(e, n - 1);
+      en = pick<KP>(e, n) + w * e1;
+      pi = w * e1 / en;
+    }
+    float* row = pi_joint + (b * (int64_t)gmax + lane) * gmax;
+    for (int j = 0; j < gmax; ++j) {
+      const double wj = readlane_d(w, j < g ? j : 0), pj = readlane_d(pi, j < g ? j : 0);
+      double v = 0.0;
+      if (unit && j < g) {
+        if (j == lane) {
+          v = pi;
+        } else if (fabs(wj - w) > 0.01 * fmax(wj, w)) {
+          v = (wj * pi - w * pj) / (wj - w);
+        } else if (n >= 2) {
+          double e2[KP];
+          esp_excl<KP>(w, g, n - 2, lane, j, e2);   // w of lane j is excluded too
+          v = w * wj * pick<KP>(e2, n - 2) / en;
+        }
+      }
+      if (lane < gmax) row[j] = (float)v;
+    }
+  }
+}
+
+template <int KP>
+__global__ __launch_bounds__(kWave) void cps_draw_kernel(
+    int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets,
+    const double* __restrict__ w, const int32_t* __restrict__ n_in, uint64_t seed, int64_t rep0,
+    int64_t R, int64_t nwg, uint8_t* __restrict__ mask, int32_t* __restrict__ edge_count,
+    int32_t* d_status) {
+  __shared__ double E[(KP + 1) * (KP + 1)];   // E[i][k], row stride KP + 1
+  __shared__ double wl[KP];
+  const int64_t b = blockIdx.x / nwg;
+  const int64_t chunk = blockIdx.x - b * nwg;
+  const int lane = threadIdx.x;
+  int64_t o0, g64;
+  if (!prompt_bounds(offsets, b, nv, 1, gmax, &o0, &g64, d_status, chunk == 0 && lane == 0))
+    return;
+  const int g = (int)g64;
+  const int n = n_in[b];
+  bool bad = n < 0 || n > g;
+  if (!bad && lane < g) {
+    const double wv = w[o0 + lane];
+    bad = !(wv > 0.0 && wv < 1e300);
+    wl[lane] = wv;
+  }
+  if (__ballot(bad) != 0ull) {
+    if (chunk == 0 && lane == 0) raise_status(d_status, PAIR_ST_P_RANGE);
+    return;
+  }
+  constexpr int S = KP + 1;
+  const bool all_or_none = n == 0 || n == g;   // no randomness: the table is not needed
+  if (!all_or_none) {
+    if (lane <= n) E[g * S + lane] = lane == 0 ? 1.0 : 0.0;
+  }
+  __syncthreads();
+  for (int i = all_or_none ? -1 : g - 1; i >= 0; --i) {
+    if (lane <= n) {
+      double v = 1.0;
+      if (lane >= 1) {
+        const double tmul = __dmul_rn(wl[i], E[(i + 1) * S + lane - 1]);
+        v = __dadd_rn(E[(i + 1) * S + lane], tmul);
+      }
+      E[i * S + lane] = v;
+    }
+    __syncthreads();
+  }
+
+  const int64_t r = chunk * kWave + lane;
+  if (r >= R) return;
+  const uint64_t rg = (uint64_t)(rep0 + r);
+  uint8_t* mrow = mask + r * nv + o0;
+  int k = n;
+  Philox4x64 x;
+  for (int i = 0; i < g; ++i) {
+    if (all_or_none) {
+      mrow[i] = (uint8_t)(n == g ? 1 : 0);
+      continue;
+    }
+    if ((i & 3) == 0) x = philox4x64_10(rg, (uint64_t)b, (uint64_t)(i >> 2), 0ull, seed, 0ull);
+    const double u = (double)(philox_word(x, i & 3) >> 32);
+    int take = 0;
+    if (k > 0) {
+      const double num = __dmul_rn(wl[i], E[(i + 1) * S + k - 1]);
+      const double prob = __ddiv_rn(num, E[i * S + k]);
+      take = u < __dmul_rn(prob, 4294967296.0) ? 1 : 0;
+    }
+    mrow[i] = (uint8_t)take;
+    k -= take;
+  }
+  if (edge_count != nullptr) edge_count[r * B + b] = n * (n - 1) / 2;
+}
+
+}  // namespace
+
+int launch_cps_fit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                   const float* pi_target, double* w, int32_t* n_out, float* pi_joint,
+                   int32_t* iters, int32_t* d_status, hipStream_t stream) {
+  const int ks = (gmax + 15) / 16;
+#define PAIR_CPS_FIT(KP_)                                                                        \
+  hipLaunchKernelGGL(cps_fit_kernel<KP_>, dim3((unsigned)B), dim3(kWave), 0, stream, B, nv, gmax, \
+                     offsets, pi_target, w, n_out, pi_joint, iters, d_status)
+  switch (ks) {
+    case 1: PAIR_CPS_FIT(16); break;
+    case 2: PAIR_CPS_FIT(32); break;
+    case 3: PAIR_CPS_FIT(48); break;
+    default: PAIR_CPS_FIT(64); break;
+  }
+#undef PAIR_CPS_FIT
+  return hipGetLastError() == hipSuccess ? PAIR_OK : PAIR_EHIP;
+}
+
+int launch_cps_draw(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, const double* w,
+                    const int32_t* n, uint64_t seed, int64_t rep0, int64_t R, uint8_t* mask,
+                    int32_t* edge_count, int32_t* d_status, hipStream_t stream) {
+  const int ks = (gmax + 15) / 16;
+  const int64_t nwg = (R + kWave - 1) / kWave;
+  const int64_t grid = B * nwg;
+  if (grid > 0x7fffffffLL) return PAIR_ERANGE;
+#define PAIR_CPS_DRAW(KP_)                                                                     \
+  hipLaunchKernelGGL(cps_draw_kernel<KP_>, dim3((unsigned)grid), dim3(kWave), 0, stream, B, nv, \
+                     gmax, offsets, w, n, seed, rep0, R, nwg, mask, edge_count, d_status)
+  switch (ks) {
+    case 1: PAIR_CPS_DRAW(16); break;
+    case 2: PAIR_CPS_DRAW(32); break;
+    case 3: PAIR_CPS_DRAW(48); break;
+    default: PAIR_CPS_DRAW(64); break;
+  }
+#undef PAIR_CPS_DRAW
+  return hipGetLastError() == hipSuccess ? PAIR_OK : PAIR_EHIP;
+}
+
+}  // namespace pair

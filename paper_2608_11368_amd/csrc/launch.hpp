@@ -38,6 +38,14 @@ int launch_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, co
                  int32_t design, float* pi, double* objective, int32_t* iters, int32_t* d_status,
                  hipStream_t stream);
 
+int launch_cps_fit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                   const float* pi_target, double* w, int32_t* n_out, float* pi_joint,
+                   int32_t* iters, int32_t* d_status, hipStream_t stream);
+
+int launch_cps_draw(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, const double* w,
+                    const int32_t* n, uint64_t seed, int64_t rep0, int64_t R, uint8_t* mask,
+                    int32_t* edge_count, int32_t* d_status, hipStream_t stream);
+
 size_t exact_workspace_bytes(int64_t B, int32_t gmax, int64_t D);
 
 int launch_audit_exact(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,

@@ -178,6 +178,38 @@ def alloc_inputs(w: Workload, offsets: np.ndarray, ratio: float = 0.5,
     return AllocInputs(p_hat=p_hat, c_hat=c_hat, budget=budget)
 
 
+def cps_targets(offsets: np.ndarray, seed: int = 4242, lo: float = 0.08, hi: float = 0.92
+                ) -> np.ndarray:
+    """Target first-order probabilities for the fixed-size design: uniform on
+    [lo, hi] per candidate, then scaled within each prompt so that the sum is
+    the nearest admissible integer n (1 <= n < G), all values staying below 1.
+    float32 [nv]."""
+    rng = np.random.default_rng(seed)
+    out = np.zeros(int(offsets[-1]), dtype=np.float32)
+    for b in range(offsets.size - 1):
+        lo_i, hi_i = int(offsets[b]), int(offsets[b + 1])
+        g = hi_i - lo_i
+        while True:
+            t = rng.uniform(lo, hi, g)
+            n = int(min(max(round(t.sum()), 1), g - 1))
+            t = t * (n / t.sum())
+            if t.max() < 0.97:
+                break
+        out[lo_i:hi_i] = t.astype(np.float32)
+    return out
+
+
+def cps_odds(offsets: np.ndarray, seed: int = 777) -> tuple[np.ndarray, np.ndarray]:
+    """Synthetic odds (float64 [nv], LogNormal(0, 1)) and sample sizes
+    (int32 [B], uniform on 1..G-1) for the fixed-size draw."""
+    rng = np.random.default_rng(seed)
+    nv = int(offsets[-1])
+    w = rng.lognormal(0.0, 1.0, nv)
+    n = np.array([rng.integers(1, int(offsets[b + 1] - offsets[b]))
+                  for b in range(offsets.size - 1)], dtype=np.int32)
+    return w, n
+
+
 def score_scale(w: Workload) -> float:
     return 1.0 if w.score_std == "unit" else 1.0 / math.sqrt(w.D)
 
