@@ -240,6 +240,46 @@ def time_alloc(pair, stream, wl, dev, reps=5):
     return out
 
 
+def time_cps(pair, stream, wl, dev, reps=5, R=1):
+    """Fixed-size conditional Poisson design on the ragged workload's prompt
+    structure (B = 512, G_b ~ U{2..64}): the odds fit with the exact joint
+    block, and one draw of every prompt, timed with events."""
+    import torch
+
+    w = wl.WORKLOADS["ragged"]
+    meta = wl.host_meta(w)
+    tgt = torch.from_numpy(wl.cps_targets(meta.offsets)).to(dev)
+    off = torch.from_numpy(meta.offsets).to(dev)
+    B, nv, G = meta.B, meta.nv, meta.gmax
+    wv = torch.empty(nv, dtype=torch.float64, device=dev)
+    n = torch.empty(B, dtype=torch.int32, device=dev)
+    pj = torch.empty((B, G, G), dtype=torch.float32, device=dev)
+    its = torch.empty(B, dtype=torch.int32, device=dev)
+    mask = torch.empty((R, nv), dtype=torch.uint8, device=dev)
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+    res = {"workload": f"B={B}, G_b~U{{2..64}}, nv={nv}, targets U[0.08, 0.92] scaled to an "
+                       "integer sum"}
+    with torch.cuda.stream(stream):
+        for name, fn in (("fit_ms", lambda: pair.pair_cps_fit(B, nv, G, off, tgt, wv, n, pj, its,
+                                                              st, stream)),
+                         ("draw_ms", lambda: pair.pair_cps_draw(B, nv, G, off, wv, n, 7, 0, R,
+                                                                mask, None, st, stream))):
+            fn()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            e1.synchronize()
+            res[name] = round(e0.elapsed_time(e1) / reps, 4)
+    res["fit_iters_mean"] = round(float(its.float().mean().item()), 1)
+    res["fit_iters_max"] = int(its.max().item())
+    if int(st.item()) != 0:
+        raise RuntimeError(f"device status {int(st.item())} in the fixed-size design")
+    return res
+
+
 def time_exact_audit(pair, stream, B, nv, G, off, scores, rew, p, D, reps=10):
     """Exact design audit (Gram on the matrix cores + closed form) on the
     audit workload, timed with events on the launch stream.  HBM-bound: the
@@ -504,6 +544,7 @@ def main():
     result["exact_audit"] = time_exact_audit(pair, stream, Ba, nva, Ga, off_a, scores_a, rew_a,
                                              p_a, Da)
     result["design_alloc"] = time_alloc(pair, stream, wl, dev)
+    result["fixed_size_design"] = time_cps(pair, stream, wl, dev)
     result["variants"] = time_variants(pair, stream, B, nv, G, off, rew, mask, pi, coeff,
                                        (Ba, nva, Ga, off_a, scores_a, rew_a, p_a, wa, R, mse, bias,
                                         reps, ec_a, ws), status)

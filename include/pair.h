@@ -169,7 +169,8 @@ int pair_design_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offset
  * first-order probability pi_target_i (the target is scaled by n_b / sum to
  * sum to n_b exactly).  Samples S of size n_b have probability
  * prod_{i in S} w_i / e_n(w) with odds w fitted here in fp64 (multiplicative
- * fixed point w_i <- w_i pi_target_i / pi_i(w), to 1e-12 relative), and the
+ * fixed point w_i <- w_i (pi_target_i / pi_i(w))^alpha, over-relaxed until
+ * the error first grows, to 1e-12 relative), and the
  * exact joint probabilities
  *     pi_ij = w_i w_j e_{n-2}(w without i, j) / e_n(w)
  * do not factorise; they are what the estimator must weight with.

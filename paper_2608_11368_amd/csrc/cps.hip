@@ -10,14 +10,19 @@
 //     pi_ij = w_i w_j e_{n-2}(w without i, j) / e_n(w)
 //           = (w_j pi_i - w_i pi_j) / (w_j - w_i)          (w_i != w_j).
 //
-//  cps_fit_kernel   one wavefront per prompt, lane i = unit i, fp64.  Each
-//                   lane keeps its leave-one-out polynomial e_k(w without i),
-//                   k <= n, in registers (the recursion over units adds
-//                   w_m e_{k-1} into e_k, with w_m = 0 for m = i, which adds
-//                   exactly nothing); the odds follow the multiplicative fixed
-//                   point w_i <- w_i pi_target_i / pi_i(w), renormalised to a
-//                   geometric mean of 1, until every pi_i is within 1e-12 of
-//                   its target.  The joint block uses the difference formula
+//  cps_fit_kernel   one wavefront per prompt, fp64.  Each iteration builds the
+//                   prefix polynomials e_k(w_0..w_{m-1}) and the suffix
+//                   polynomials e_k(w_{m+1}..w_{G-1}) for all m (lane k holds
+//                   coefficient k; adding a unit is one whole-wave DPP shift
+//                   and one multiply-add), and lane i gets the leave-one-out
+//                   coefficient e_{n-1}(w without i) as the convolution
+//                   sum_k prefix_i[k] suffix_i[n-1-k] (all terms positive);
+//                   the odds follow the multiplicative fixed point
+//                   w_i <- w_i (pi_target_i / pi_i(w))^alpha, over-relaxed
+//                   with alpha = 1.8 until the error first grows and with
+//                   alpha = 1 from then on, renormalised to a geometric mean
+//                   of 1, until every pi_i is within 1e-12 of its target
+//                   (the fixed point is the same for every alpha).  The joint block uses the difference formula
 //                   when the two odds differ by more than 1% and the direct
 //                   leave-two-out polynomial otherwise.
 //  cps_draw_kernel  lane = replicate.  The workgroup builds the suffix table
@@ -69,11 +74,40 @@ __device__ __forceinline__ uint64_t philox_word(const Philox4x64& x, int q) {
   return q == 0 ? x.w[0] : (q == 1 ? x.w[1] : (q == 2 ? x.w[2] : x.w[3]));
 }
 
+// Prefix rows Pf[m][k] = e_k(w_0 .. w_{m-1}), m = 0..g, and suffix rows
+// Sf[m][k] = e_k(w_{m+1} .. w_{g-1}), m = 0..g-1, for k <= n, written to LDS
+// with row stride kS.  Lane k carries coefficient k; adding unit m is
+// e_k <- e_k + w_m e_{k-1}, where e_{k-1} arrives from lane k - 1 by a
+// whole-wave DPP shift (lane 0 receives 0).
+constexpr int kS = 65;
+
+template <int KP>
+__device__ __forceinline__ void esp_tables(double w, int g, int n, int lane, double* Pf,
+                                           double* Sf) {
+  double col = lane == 0 ? 1.0 : 0.0;
+  if (lane <= n) Pf[lane] = col;
+  for (int m = 0; m < g; ++m) {
+    const double wm = readlane_d(w, m);
+    col = __dadd_rn(col, __dmul_rn(wm, dpp_d<0x138>(col)));   // wave_shr:1
+    if (lane <= n) Pf[(m + 1) * kS + lane] = col;
+  }
+  col = lane == 0 ? 1.0 : 0.0;
+  if (lane <= n) Sf[(g - 1) * kS + lane] = col;
+  for (int m = g - 1; m >= 1; --m) {
+    const double wm = readlane_d(w, m);
+    col = __dadd_rn(col, __dmul_rn(wm, dpp_d<0x138>(col)));
+    if (lane <= n) Sf[(m - 1) * kS + lane] = col;
+  }
+  __syncthreads();
+}
+
 template <int KP>
 __global__ __launch_bounds__(kWave) void cps_fit_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets,
     const float* __restrict__ pi_target, double* __restrict__ w_out, int32_t* __restrict__ n_out,
     float* __restrict__ pi_joint, int32_t* __restrict__ iters, int32_t* d_status) {
+  __shared__ double Pf[(KP + 1) * kS];
+  __shared__ double Sf[KP * kS];
   const int64_t b = blockIdx.x;
   const int lane = threadIdx.x;
   int64_t o0, g64;
@@ -103,22 +137,28 @@ __global__ __launch_bounds__(kWave) void cps_fit_kernel(
   double e[KP];
   int it = 0;
   bool converged = false;
+  double alpha = 1.8, prev_err = 1e300;   // over-relaxed step, back to 1 if the error grows
   for (; it < kMaxFitIter; ++it) {
-    esp_excl<KP>(w, g, n, lane, -1, e);
+    // pi_i(w) for every unit from the prefix and suffix polynomial tables.
+    esp_tables<KP>(w, g, n, lane, Pf, Sf);
     double pi = 0.0;
     if (unit) {
-      const double e1 = pick<KP>(e, n - 1);
-      const double en = pick<KP>(e, n) + w * e1;   // e_n(w) from the leave-one-out polynomial
-      pi = w * e1 / en;
+      double e1 = 0.0;   // e_{n-1}(w without i) = sum_k Pf[i][k] Sf[i][n-1-k]
+      for (int k = 0; k < n; ++k)
+        e1 = __dadd_rn(e1, __dmul_rn(Pf[lane * kS + k], Sf[lane * kS + (n - 1 - k)]));
+      pi = w * e1 / Pf[g * kS + n];
     }
     const double err = wave_max_d(unit ? fabs(pi / t - 1.0) : 0.0);
     if (err <= 1e-12) {
       converged = true;
       break;
     }
-    if (unit) w *= t / pi;
+    if (err > prev_err) alpha = 1.0;
+    prev_err = err;
+    if (unit) w *= alpha == 1.0 ? t / pi : pow(t / pi, alpha);
     const double lg = wave_sum_d(unit ? log(w) : 0.0) / (double)g;
     w = unit ? w * exp(-lg) : 0.0;
+    __syncthreads();   // the tables are rebuilt by the next iteration
   }
   if (!converged && lane == 0) raise_status(d_status, PAIR_ST_P_RANGE);
   if (unit) w_out[o0 + lane] = w;
