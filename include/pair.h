@@ -236,6 +236,27 @@ int pair_edge_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets
                      int32_t* edge_count, int32_t* d_status, void* stream);
 
 /*
+ * pair_design_coeffs -- the design draw of one replicate and the HT
+ * coefficient fold in a single launch (paper Sec. 2.3 and Eq.
+ * (pair-advantage), as pair_design_inclusion followed by pair_edge_coeffs on
+ * its logged block).  The indicators, the logged rho_ij = fl32(p_i p_j) and
+ * the coefficients are bitwise those of the two calls with R = 1 and
+ * rep0 = rep; the mask and pi block are written only if asked for.
+ *
+ *   p, rewards     fp32 [nv]
+ *   seed, rep      generator key and the replicate index
+ *   mask           uint8 [nv] out                                    (or NULL)
+ *   pi             fp32 [B][gmax][gmax] out, as pair_design_inclusion (or NULL)
+ *   coeff          fp32 [nv] out: A~
+ *   edge_count, completed  int32 [B] out                             (or NULL)
+ * Device status: PAIR_ST_BAD_GROUP, PAIR_ST_P_RANGE, PAIR_ST_RHO_RANGE.
+ */
+int pair_design_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                       const float* p, const float* rewards, uint64_t seed, int64_t rep,
+                       uint8_t* mask, float* pi, float* coeff, int32_t* edge_count,
+                       int32_t* completed, int32_t* d_status, void* stream);
+
+/*
  * pair_edge_coeffs_rule -- pair_edge_coeffs under any edge-weight rule
  * (PAIR_RULE_*), plus the per-prompt weight diagnostics the paper logs
  * (App. C "Probability optimization"; App. D metrics):

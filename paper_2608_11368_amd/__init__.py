@@ -42,7 +42,7 @@ RULE_CLIPPED = 3
 RULE_SELFNORM = 4
 RULE_MARGINAL = 5
 
-EXPORTED = ("pair_design_alloc", "pair_cps_fit", "pair_cps_draw", "pair_design_inclusion", "pair_edge_coeffs", "pair_edge_coeffs_rule",
+EXPORTED = ("pair_design_coeffs", "pair_design_alloc", "pair_cps_fit", "pair_cps_draw", "pair_design_inclusion", "pair_edge_coeffs", "pair_edge_coeffs_rule",
             "pair_weighted_grad", "pair_audit_workspace_bytes", "pair_audit", "pair_audit_rule",
             "pair_audit_exact_workspace_bytes", "pair_audit_exact", "pair_strerror",
             "pair_version")
@@ -84,6 +84,8 @@ def lib() -> ctypes.CDLL:
         L.pair_audit_exact.restype = ctypes.c_int
         L.pair_design_alloc.argtypes = [i64, i64, i32, P, P, P, P, P, f32, i32, P, P, P, P, P]
         L.pair_design_alloc.restype = ctypes.c_int
+        L.pair_design_coeffs.argtypes = [i64, i64, i32, P, P, P, u64, i64, P, P, P, P, P, P, P]
+        L.pair_design_coeffs.restype = ctypes.c_int
         L.pair_cps_fit.argtypes = [i64, i64, i32, P, P, P, P, P, P, P, P]
         L.pair_cps_fit.restype = ctypes.c_int
         L.pair_cps_draw.argtypes = [i64, i64, i32, P, P, P, u64, i64, i64, P, P, P, P]
@@ -163,6 +165,19 @@ def pair_design_inclusion(B, nv, gmax, offsets, p, seed, rep0, R, mask=None, pi=
         _dev(edge_count, "edge_count", torch.int32, R * B, True),
         _dev(completed, "completed", torch.int32, R * B, True),
         _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_design_inclusion")
+
+
+def pair_design_coeffs(B, nv, gmax, offsets, p, rewards, seed, rep, coeff, mask=None, pi=None,
+                       edge_count=None, completed=None, d_status=None, stream=None):
+    _rc(lib().pair_design_coeffs(
+        B, nv, gmax, _dev(offsets, "offsets", torch.int64, B + 1), _dev(p, "p", torch.float32, nv),
+        _dev(rewards, "rewards", torch.float32, nv), ctypes.c_uint64(seed & ((1 << 64) - 1)), rep,
+        _dev(mask, "mask", torch.uint8, nv, True),
+        _dev(pi, "pi", torch.float32, B * gmax * gmax, True),
+        _dev(coeff, "coeff", torch.float32, nv),
+        _dev(edge_count, "edge_count", torch.int32, B, True),
+        _dev(completed, "completed", torch.int32, B, True),
+        _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_design_coeffs")
 
 
 def pair_design_alloc(B, nv, gmax, offsets, p_hat, c_hat, m_hat, budget, pi_min, design, pi,

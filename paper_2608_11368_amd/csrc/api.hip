@@ -91,6 +91,18 @@ int pair_edge_coeffs_rule(int64_t B, int64_t nv, int32_t gmax, const int64_t* of
                              edge_count, ess, max_weight, d_status, as_stream(stream));
 }
 
+int pair_design_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                       const float* p, const float* rewards, uint64_t seed, int64_t rep,
+                       uint8_t* mask, float* pi, float* coeff, int32_t* edge_count,
+                       int32_t* completed, int32_t* d_status, void* stream) {
+  int st = check_groups(B, nv, gmax, offsets);
+  if (st) return st;
+  if (p == nullptr || rewards == nullptr || coeff == nullptr) return PAIR_EINVAL;
+  if (rep < 0 || rep > kMaxCount) return PAIR_ERANGE;
+  return pair::launch_design_coeffs(B, nv, gmax, offsets, p, rewards, seed, rep, mask, pi, coeff,
+                                    edge_count, completed, d_status, as_stream(stream));
+}
+
 int pair_edge_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                      const float* rewards, const uint8_t* mask, const float* pi, float* coeff,
                      int32_t* edge_count, int32_t* d_status, void* stream) {

@@ -102,6 +102,89 @@ __global__ __launch_bounds__(64) void edge_coeffs_kernel(
   }
 }
 
+// Design draw and HT coefficient fold of one replicate in one launch: one
+// wavefront per prompt, lane i = vertex i.  The indicators are drawn exactly
+// as design_draw_kernel draws them, the logged rho_ij = fl32(p_i p_j) is
+// formed on the fly (the value the design writes to its pi block), and the
+// fold adds (r_i - r_j) / rho_ij over observed partners in ascending order,
+// then centres -- the same arithmetic as edge_coeffs_kernel on the logged
+// block, so the coefficients are bitwise those of the two-call path.
+__global__ __launch_bounds__(64) void design_coeffs_kernel(
+    int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets,
+    const float* __restrict__ p, const float* __restrict__ rewards, uint64_t seed, int64_t rep,
+    uint8_t* __restrict__ mask, float* __restrict__ pi, float* __restrict__ coeff,
+    int32_t* __restrict__ edge_count, int32_t* __restrict__ completed, int32_t* d_status) {
+  const int64_t b = blockIdx.x;
+  const int lane = threadIdx.x;
+  int64_t o0, g;
+  const bool ok = prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, d_status, lane == 0);
+  if (pi != nullptr) {
+    float* blk = pi + b * (int64_t)gmax * gmax;
+    for (int idx = lane; idx < gmax * gmax; idx += kWave) {
+      const int i = idx / gmax, j = idx - i * gmax;
+      float v = 0.0f;
+      if (ok && i < g && j < g) v = (i == j) ? p[o0 + i] : p[o0 + i] * p[o0 + j];
+      blk[idx] = v;
+    }
+  }
+  if (!ok) return;
+  const bool vert = lane < g;
+  const float p_i = vert ? p[o0 + lane] : 1.0f;
+  const float r_i = vert ? rewards[o0 + lane] : 0.0f;
+  int J = 0;
+  if (vert) {
+    const Philox4x64 x = philox4x64_10((uint64_t)rep, (uint64_t)b, (uint64_t)(lane >> 2), 0ull,
+                                       seed, 0ull);
+    const uint64_t u32 = x.w[lane & 3] >> 32;
+    if (p_in_range(p_i)) {
+      J = u32 < inclusion_threshold(p_i) ? 1 : 0;
+    } else {
+      raise_status(d_status, PAIR_ST_P_RANGE);
+    }
+    if (mask != nullptr) mask[o0 + lane] = (uint8_t)J;
+  }
+  const uint64_t obs = __ballot(J != 0);
+  const int k = __popcll(obs);
+  const bool m_i = J != 0;
+  float c = 0.0f;
+  bool bad_rho = false;
+  for (int j = 0; j < g; ++j) {
+    const float r_j = __shfl(r_i, j, kWave);
+    const float p_j = __shfl(p_i, j, kWave);
+    if (!((obs >> j) & 1ull) || !m_i || j == lane) continue;
+    const float rho = lane < j ? p_i * p_j : p_j * p_i;
+    if (!(rho > 0.0f && rho <= 1.0f)) {
+      bad_rho = true;
+      continue;
+    }
+    c += (r_i - r_j) / rho;
+  }
+  if (bad_rho) raise_status(d_status, PAIR_ST_RHO_RANGE);
+  float a = 0.0f;
+  if (m_i && k >= 2) a = c / (float)(g * (g - 1));
+  const float total = wave_sum(a);
+  if (k >= 2 && m_i) {
+    a = a - total / (float)k;
+  } else {
+    a = 0.0f;
+  }
+  if (vert) coeff[o0 + lane] = a;
+  if (lane == 0) {
+    if (edge_count != nullptr) edge_count[b] = k * (k - 1) / 2;
+    if (completed != nullptr) completed[b] = k;
+  }
+}
+
+int launch_design_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                         const float* p, const float* rewards, uint64_t seed, int64_t rep,
+                         uint8_t* mask, float* pi, float* coeff, int32_t* edge_count,
+                         int32_t* completed, int32_t* d_status, hipStream_t stream) {
+  hipLaunchKernelGGL(design_coeffs_kernel, dim3((unsigned)B), dim3(64), 0, stream, B, nv, gmax,
+                     offsets, p, rewards, seed, rep, mask, pi, coeff, edge_count, completed,
+                     d_status);
+  return hipGetLastError() == hipSuccess ? PAIR_OK : PAIR_EHIP;
+}
+
 int launch_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                   const float* rewards, const uint8_t* mask, const float* pi, int32_t rule,
                   float wmax, float* coeff, int32_t* edge_count, float* ess, float* max_weight,

@@ -6,7 +6,8 @@
 // lane evaluates Philox4x64-10 at counter (r, b, i >> 2, 0) and keeps word
 // i & 3 (lanes of one group of four compute the same block in lockstep, so
 // this costs one generator evaluation per unit).  Completed-vertex and edge
-// counts come from a ballot + popcount.
+// counts come from a ballot + popcount.  The waves of replicate 0 also write
+// their prompt's logged rho block, so one launch serves both outputs.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -15,16 +16,30 @@ namespace pair {
 __global__ __launch_bounds__(256) void design_draw_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets,
     const float* __restrict__ p, uint64_t seed, int64_t rep0, int64_t R, uint8_t* __restrict__ mask,
-    int32_t* __restrict__ edge_count, int32_t* __restrict__ completed, int32_t* d_status) {
+    float* __restrict__ pi, int32_t* __restrict__ edge_count, int32_t* __restrict__ completed,
+    int32_t* d_status) {
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t units = B * R;
   const int64_t waves_total = (int64_t)gridDim.x * (blockDim.x / kWave);
+  const bool draws = mask != nullptr || edge_count != nullptr || completed != nullptr;
   for (int64_t u = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave; u < units;
        u += waves_total) {
     const int64_t r = u / B;  // replicate-major: consecutive waves share r
     const int64_t b = u - r * B;
     int64_t o0, g;
-    if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, d_status, r == 0)) continue;
+    const bool ok = prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, d_status, r == 0);
+    if (r == 0 && pi != nullptr) {
+      // Logged rho block: fl32(p_i p_j) off the diagonal, p_i on it, zero
+      // outside the G_b x G_b corner (all zero for a malformed prompt).
+      float* blk = pi + b * (int64_t)gmax * gmax;
+      for (int idx = lane; idx < gmax * gmax; idx += kWave) {
+        const int i = idx / gmax, j = idx - i * gmax;
+        float v = 0.0f;
+        if (ok && i < g && j < g) v = (i == j) ? p[o0 + i] : p[o0 + i] * p[o0 + j];
+        blk[idx] = v;
+      }
+    }
+    if (!ok || !draws) continue;
     const bool active = lane < g;
     int J = 0;
     if (active) {
@@ -48,45 +63,18 @@ __global__ __launch_bounds__(256) void design_draw_kernel(
   }
 }
 
-// Logged rho block per prompt: rho_ij = fl32(p_i * p_j) off the diagonal,
-// p_i on it, zero outside the G_b x G_b corner.
-__global__ __launch_bounds__(256) void design_pi_kernel(int64_t B, int64_t nv, int32_t gmax,
-                                                        const int64_t* __restrict__ offsets,
-                                                        const float* __restrict__ p,
-                                                        float* __restrict__ pi) {
-  const int64_t b = blockIdx.x;
-  if (b >= B) return;
-  const int64_t a = offsets[b], e = offsets[b + 1];
-  const bool ok = a >= 0 && e >= a && e <= nv && (e - a) >= 2 && (e - a) <= gmax;
-  const int64_t g = ok ? e - a : 0;
-  const int64_t n = (int64_t)gmax * gmax;
-  float* blk = pi + b * n;
-  for (int64_t idx = threadIdx.x; idx < n; idx += blockDim.x) {
-    const int64_t i = idx / gmax, j = idx - i * gmax;
-    float v = 0.0f;
-    if (i < g && j < g) v = (i == j) ? p[a + i] : p[a + i] * p[a + j];
-    blk[idx] = v;
-  }
-}
-
 int launch_design(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, const float* p,
                   uint64_t seed, int64_t rep0, int64_t R, uint8_t* mask, float* pi,
                   int32_t* edge_count, int32_t* completed, int32_t* d_status, hipStream_t stream) {
-  if (pi != nullptr) {
-    hipLaunchKernelGGL(design_pi_kernel, dim3((unsigned)B), dim3(256), 0, stream, B, nv, gmax,
-                       offsets, p, pi);
-    if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
-  }
-  if (mask != nullptr || edge_count != nullptr || completed != nullptr) {
-    const int64_t units = B * R;
-    const int64_t blocks_needed = (units + 3) / 4;
-    const int64_t cap = (int64_t)device_cu_count() * 32;
-    const unsigned grid = (unsigned)(blocks_needed < cap ? blocks_needed : cap);
-    hipLaunchKernelGGL(design_draw_kernel, dim3(grid), dim3(256), 0, stream, B, nv, gmax, offsets,
-                       p, seed, rep0, R, mask, edge_count, completed, d_status);
-    if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
-  }
-  return PAIR_OK;
+  const bool draws = mask != nullptr || edge_count != nullptr || completed != nullptr;
+  if (!draws && pi == nullptr) return PAIR_OK;
+  const int64_t units = draws ? B * R : B;   // the rho block needs replicate 0 only
+  const int64_t blocks_needed = (units + 3) / 4;
+  const int64_t cap = (int64_t)device_cu_count() * 32;
+  const unsigned grid = (unsigned)(blocks_needed < cap ? blocks_needed : cap);
+  hipLaunchKernelGGL(design_draw_kernel, dim3(grid), dim3(256), 0, stream, B, nv, gmax, offsets, p,
+                     seed, rep0, draws ? R : 1, mask, pi, edge_count, completed, d_status);
+  return hipGetLastError() == hipSuccess ? PAIR_OK : PAIR_EHIP;
 }
 
 }  // namespace pair

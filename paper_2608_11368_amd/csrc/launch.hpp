@@ -20,6 +20,11 @@ int launch_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                   float wmax, float* coeff, int32_t* edge_count, float* ess, float* max_weight,
                   int32_t* d_status, hipStream_t stream);
 
+int launch_design_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                         const float* p, const float* rewards, uint64_t seed, int64_t rep,
+                         uint8_t* mask, float* pi, float* coeff, int32_t* edge_count,
+                         int32_t* completed, int32_t* d_status, hipStream_t stream);
+
 int launch_wgrad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D, const void* scores,
                  int32_t dtype, int64_t ld, const float* coeff, float* out, int32_t reduce,
                  int32_t* d_status, hipStream_t stream);

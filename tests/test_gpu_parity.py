@@ -228,6 +228,31 @@ def test_full_size_sampled_columns(name, ncols):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("name,B", [("b128", 128), ("ragged", 512), ("tiny", 4)])
+def test_fused_design_coeffs_is_bitwise_the_two_calls(name, B):
+    w = wl.WORKLOADS[name].replace(B=B)
+    meta = wl.host_meta(w)
+    dm = upload_meta(meta)
+    log(f"fused design + coefficients {name} B={B}")
+    d = pair.design_inclusion(dm["offsets"], dm["p"], w.design_seed, 3, 1, meta.gmax, nv=meta.nv)
+    c = pair.edge_coeffs(dm["offsets"], dm["rewards"], d["mask"][0], d["pi"], meta.gmax, nv=meta.nv)
+    coeff = torch.empty(meta.nv, device=DEV)
+    mask = torch.empty(meta.nv, dtype=torch.uint8, device=DEV)
+    pi = torch.empty((meta.B, meta.gmax, meta.gmax), device=DEV)
+    ec = torch.empty(meta.B, dtype=torch.int32, device=DEV)
+    comp = torch.empty(meta.B, dtype=torch.int32, device=DEV)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    pair.pair_design_coeffs(meta.B, meta.nv, meta.gmax, dm["offsets"], dm["p"], dm["rewards"],
+                            w.design_seed, 3, coeff, mask, pi, ec, comp, st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    assert torch.equal(mask, d["mask"][0]) and torch.equal(pi, d["pi"])
+    assert torch.equal(coeff, c["coeff"])
+    assert torch.equal(ec, d["edge_count"][0]) and torch.equal(comp, d["completed"][0])
+    od = oracle.design_inclusion(meta.offsets, meta.p, w.design_seed, 3, 1, meta.gmax)
+    assert np.array_equal(mask.cpu().numpy(), od["mask"][0])
+
+
 # ------------------------------------------- weighted gradient, batch mean --
 def test_weighted_grad_mean_tiny_fp32():
     w = wl.WORKLOADS["tiny"]
