@@ -196,10 +196,86 @@ def cpu_baseline(meta, w, scores_dev, meta_a, wa, scores_a_dev, budget_s=12.0):
         "audit_value": reps / da,
         "audit_unit": "replicate-estimates/s",
         "seconds": dt + da,
+        "cpu_model": _cpu_model(),
     }
 
 
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 RULE_NAMES = ("ht", "unweighted", "ratio_ke", "clipped", "selfnorm", "marginal")
+
+
+def _event_ms(stream, fn, reps):
+    import torch
+
+    fn()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    e1.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def time_wgrad_configs(pair, stream, wl, dev, coeff, out, scores, off, rew, p, mask, pi, ec, comp,
+                       status, B, nv, G, D, w):
+    """The weighted-gradient stream beyond the headline workload: the b128
+    batch-mean reduce mode (score bytes are nearly all its traffic), and the
+    per-prompt mode on the Qwen3-shaped slice (B=64, G=8, D=2^26, 68.7 GB of
+    bf16 scores) and on the ragged workload (B=512, G_b ~ U{2..64}, D=2^18).
+    GB/s of algorithmic bytes (nonzero score rows, coefficients, offsets,
+    output), kernel timed alone with events on the launch stream."""
+    import torch
+
+    res = {}
+    with torch.cuda.stream(stream):
+        mean = torch.empty(D, dtype=torch.float32, device=dev)
+        nz = int(torch.count_nonzero(coeff).item())
+        ms = _event_ms(stream, lambda: pair.pair_weighted_grad(B, nv, off, scores, coeff, mean, 1,
+                                                                status, stream), 10)
+        alg = nz * D * 2 + nv * 4 + (B + 1) * 8 + D * 4
+        res["b128_batch_mean"] = {"ms": round(ms, 4), "GBps": round(alg / ms / 1e6, 1),
+                                  "frac": round(alg / ms / 1e6 / HBM_PEAK_GBPS, 4)}
+    del mean
+    for name in ("qwen3", "ragged"):
+        wk = wl.WORKLOADS[name]
+        meta = wl.host_meta(wk)
+        _log(f"[bench] generating {name} scores {meta.nv}x{wk.D} bf16")
+        s_k = wl.device_scores(wk, meta.nv, dev)
+        o_k = torch.from_numpy(meta.offsets).to(dev)
+        r_k = torch.from_numpy(meta.rewards).to(dev)
+        p_k = torch.from_numpy(meta.p).to(dev)
+        c_k = torch.empty(meta.nv, dtype=torch.float32, device=dev)
+        out_k = torch.empty((meta.B, wk.D), dtype=torch.float32, device=dev)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            pair.pair_design_coeffs(meta.B, meta.nv, meta.gmax, o_k, p_k, r_k, wk.design_seed, 0,
+                                    c_k, None, None, None, None, status, stream)
+            reps = 3 if wk.D > (1 << 24) else 10
+            ms = _event_ms(stream, lambda: pair.pair_weighted_grad(
+                meta.B, meta.nv, o_k, s_k, c_k, out_k, 0, status, stream), reps)
+        nz = int(torch.count_nonzero(c_k).item())
+        alg = nz * wk.D * 2 + meta.nv * 4 + (meta.B + 1) * 8 + meta.B * wk.D * 4
+        res[name] = {"B": meta.B, "nv": meta.nv, "D": wk.D, "rows_nonzero": nz,
+                     "ms": round(ms, 4), "GBps": round(alg / ms / 1e6, 1),
+                     "score_only_GBps": round(nz * wk.D * 2 / ms / 1e6, 1),
+                     "frac": round(alg / ms / 1e6 / HBM_PEAK_GBPS, 4)}
+        del s_k, out_k
+        torch.cuda.empty_cache()
+    if int(status.item()) != 0:
+        raise RuntimeError(f"device status {int(status.item())} in the gradient configurations")
+    return res
 
 
 def time_alloc(pair, stream, wl, dev, reps=5):
@@ -540,10 +616,14 @@ def main():
         "parts_ms": {"design_coeffs": round(ms_design, 4), "wgrad": round(ms_wgrad, 4),
                      "audit": round(ms_audit, 4)},
         "dense_equiv_GBps": round(bytes_dense / (ms_chain * 1e-3) / 1e9, 1),
+        "score_only_GBps": round(nz_rows * D * 2 / (ms_wgrad * 1e-3) / 1e9, 1),
         "roofline": roof_w,
         "audit": {"value": round(Ba * R / (ms_audit * 1e-3), 1),
                   "unit": "replicate-estimates/s", "roofline": roof_a},
     }
+    result["wgrad_configs"] = time_wgrad_configs(pair, stream, wl, dev, coeff, out, scores, off,
+                                                 rew, p, mask, pi, ec, comp, status, B, nv, G, D,
+                                                 w)
     result["exact_audit"] = time_exact_audit(pair, stream, Ba, nva, Ga, off_a, scores_a, rew_a,
                                              p_a, Da)
     result["design_alloc"] = time_alloc(pair, stream, wl, dev)
