@@ -604,8 +604,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
-        "accumulate": "f32",
+        "dtype": "f32",
+        "score_dtype": "bf16",
         "data": "synthetic",
         "config": {
             "workload": "b128 gradient chain + audit",
