@@ -137,7 +137,7 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
     // and rho = 1, centred over all G vertices.
     float cf = 0.0f;
     for (int j = 0; j < g; ++j) {
-      const float r_j = __shfl(r_i, j, kWave);
+      const float r_j = lane_value(r_i, j);
       if (vert && j != lane) cf += r_i - r_j;
     }
     float a_full = vert ? cf / (float)(g * (g - 1)) : 0.0f;

@@ -56,7 +56,7 @@ __global__ __launch_bounds__(64) void edge_coeffs_kernel(
   float c = 0.0f, nsn = 0.0f, sw = 0.0f, sw2 = 0.0f, wmx = 0.0f;
   bool bad_rho = false;
   for (int j = 0; j < g; ++j) {
-    const float r_j = __shfl(r_i, j, kWave);
+    const float r_j = lane_value(r_i, j);
     if (!((obs >> j) & 1ull) || !m_i || j == lane) continue;
     float rho = 1.0f, pij = 1.0f;
     if (pi != nullptr) {
@@ -109,6 +109,9 @@ __global__ __launch_bounds__(64) void edge_coeffs_kernel(
 // fold adds (r_i - r_j) / rho_ij over observed partners in ascending order,
 // then centres -- the same arithmetic as edge_coeffs_kernel on the logged
 // block, so the coefficients are bitwise those of the two-call path.
+// The kernel is one latency chain, so each lane reads its p_i and r_i once;
+// partners' values move between lanes (scalar lane reads in the fold,
+// shuffles for the rho block), and the rho block is written last.
 __global__ __launch_bounds__(64) void design_coeffs_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets,
     const float* __restrict__ p, const float* __restrict__ rewards, uint64_t seed, int64_t rep,
@@ -118,16 +121,13 @@ __global__ __launch_bounds__(64) void design_coeffs_kernel(
   const int lane = threadIdx.x;
   int64_t o0, g;
   const bool ok = prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, d_status, lane == 0);
-  if (pi != nullptr) {
-    float* blk = pi + b * (int64_t)gmax * gmax;
-    for (int idx = lane; idx < gmax * gmax; idx += kWave) {
-      const int i = idx / gmax, j = idx - i * gmax;
-      float v = 0.0f;
-      if (ok && i < g && j < g) v = (i == j) ? p[o0 + i] : p[o0 + i] * p[o0 + j];
-      blk[idx] = v;
+  if (!ok) {
+    if (pi != nullptr) {   // a malformed prompt logs an all-zero block
+      float* blk = pi + b * (int64_t)gmax * gmax;
+      for (int idx = lane; idx < gmax * gmax; idx += kWave) blk[idx] = 0.0f;
     }
+    return;
   }
-  if (!ok) return;
   const bool vert = lane < g;
   const float p_i = vert ? p[o0 + lane] : 1.0f;
   const float r_i = vert ? rewards[o0 + lane] : 0.0f;
@@ -149,8 +149,8 @@ __global__ __launch_bounds__(64) void design_coeffs_kernel(
   float c = 0.0f;
   bool bad_rho = false;
   for (int j = 0; j < g; ++j) {
-    const float r_j = __shfl(r_i, j, kWave);
-    const float p_j = __shfl(p_i, j, kWave);
+    const float r_j = lane_value(r_i, j);
+    const float p_j = lane_value(p_i, j);
     if (!((obs >> j) & 1ull) || !m_i || j == lane) continue;
     const float rho = lane < j ? p_i * p_j : p_j * p_i;
     if (!(rho > 0.0f && rho <= 1.0f)) {
@@ -172,6 +172,23 @@ __global__ __launch_bounds__(64) void design_coeffs_kernel(
   if (lane == 0) {
     if (edge_count != nullptr) edge_count[b] = k * (k - 1) / 2;
     if (completed != nullptr) completed[b] = k;
+  }
+  if (pi != nullptr) {
+    // Logged rho block: fl32(p_i p_j) off the diagonal, p_i on it, zero
+    // outside the G_b x G_b corner.
+    float* blk = pi + b * (int64_t)gmax * gmax;
+    // Whole-wave iterations: every lane takes part in the shuffles (a
+    // shuffle from an inactive lane is not defined), only the store is
+    // guarded.
+    for (int base = 0; base < gmax * gmax; base += kWave) {
+      const int idx = base + lane;
+      const int i = idx / gmax, j = idx - i * gmax;
+      const float pa = __shfl(p_i, i < kWave ? i : 0, kWave);
+      const float pb = __shfl(p_i, j, kWave);
+      float v = 0.0f;
+      if (i < g && j < g) v = (i == j) ? pa : pa * pb;
+      if (idx < gmax * gmax) blk[idx] = v;
+    }
   }
 }
 

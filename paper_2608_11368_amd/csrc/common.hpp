@@ -84,6 +84,12 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// Value of `v` in lane `j` for a wave-uniform j (a scalar read of one lane,
+// no LDS round trip).
+__device__ __forceinline__ float lane_value(float v, int j) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), j));
+}
+
 // Butterfly sum across the 64 lanes: every lane ends with the same bits
 // (IEEE addition is commutative, so partner lanes form identical sums).
 __device__ __forceinline__ float wave_sum(float v) {

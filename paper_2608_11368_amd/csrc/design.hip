@@ -28,22 +28,27 @@ __global__ __launch_bounds__(256) void design_draw_kernel(
     const int64_t b = u - r * B;
     int64_t o0, g;
     const bool ok = prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, d_status, r == 0);
+    const bool active = ok && lane < g;
+    const float pv = active ? p[o0 + lane] : 1.0f;
     if (r == 0 && pi != nullptr) {
       // Logged rho block: fl32(p_i p_j) off the diagonal, p_i on it, zero
       // outside the G_b x G_b corner (all zero for a malformed prompt).
+      // Whole-wave iterations so that every lane takes part in the shuffles
+      // of p; only the store is guarded.
       float* blk = pi + b * (int64_t)gmax * gmax;
-      for (int idx = lane; idx < gmax * gmax; idx += kWave) {
+      for (int base = 0; base < gmax * gmax; base += kWave) {
+        const int idx = base + lane;
         const int i = idx / gmax, j = idx - i * gmax;
+        const float pa = __shfl(pv, i < kWave ? i : 0, kWave);
+        const float pb = __shfl(pv, j, kWave);
         float v = 0.0f;
-        if (ok && i < g && j < g) v = (i == j) ? p[o0 + i] : p[o0 + i] * p[o0 + j];
-        blk[idx] = v;
+        if (ok && i < g && j < g) v = (i == j) ? pa : pa * pb;
+        if (idx < gmax * gmax) blk[idx] = v;
       }
     }
     if (!ok || !draws) continue;
-    const bool active = lane < g;
     int J = 0;
     if (active) {
-      const float pv = p[o0 + lane];
       const Philox4x64 x = philox4x64_10((uint64_t)(rep0 + r), (uint64_t)b, (uint64_t)(lane >> 2),
                                          0ull, seed, 0ull);
       const uint64_t u32 = x.w[lane & 3] >> 32;

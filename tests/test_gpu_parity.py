@@ -82,6 +82,32 @@ def test_design_draw_bit_exact(name, B, R, rep0):
     assert int(got["status"].item()) == 0
 
 
+@pytest.mark.parametrize("gmax", [10, 63, 64])
+def test_design_rho_block_odd_gmax(gmax):
+    """The logged rho block is written in whole-wave passes over gmax^2
+    entries; gmax^2 not a multiple of 64 leaves a partial last pass."""
+    w = wl.WORKLOADS["ragged"].replace(B=96, gmax_ragged=gmax)
+    meta = wl.host_meta(w)
+    assert meta.gmax == gmax
+    log(f"design rho block gmax={gmax} B={meta.B}")
+    dm = upload_meta(meta)
+    got = pair.design_inclusion(dm["offsets"], dm["p"], w.design_seed, 2, 2, gmax, nv=meta.nv)
+    want = oracle.design_inclusion(meta.offsets, meta.p, w.design_seed, 2, 2, gmax)
+    assert np.array_equal(got["pi"].cpu().numpy(), want["pi"])
+    assert np.array_equal(got["mask"].cpu().numpy(), want["mask"])
+    coeff = torch.empty(meta.nv, device=DEV)
+    mask = torch.empty(meta.nv, dtype=torch.uint8, device=DEV)
+    pi = torch.full((meta.B, gmax, gmax), float("nan"), device=DEV)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    pair.pair_design_coeffs(meta.B, meta.nv, gmax, dm["offsets"], dm["p"], dm["rewards"],
+                            w.design_seed, 2, coeff, mask, pi, None, None, st)
+    c = pair.edge_coeffs(dm["offsets"], dm["rewards"], got["mask"][0], got["pi"], gmax, nv=meta.nv)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0 and int(got["status"].item()) == 0
+    assert np.array_equal(pi.cpu().numpy(), want["pi"])
+    assert torch.equal(mask, got["mask"][0]) and torch.equal(coeff, c["coeff"])
+
+
 # ------------------------------------------------------ coefficient fold --
 @pytest.mark.parametrize("name", ["tiny", "b128", "ragged"])
 def test_edge_coeffs_vs_oracle(name):
