@@ -77,24 +77,38 @@ TRAFFIC_KERNELS = {
 }
 
 
+# The counter runs use `--steps 2 --warmup 1`: the first three calls of each
+# traffic kernel in dispatch order are the main loop's.
+COUNTER_RUN_STEPS = 2
+COUNTER_RUN_WARMUP = 1
+
+
 def _counter_rows(path):
     import csv
     with open(path, newline="") as f:
         return [(r["Kernel_Name"], float(r["Counter_Value"])) for r in csv.DictReader(f)]
 
 
-def _kernel_kib(rows, prefix, per_call):
-    """KiB per entry-point call: all dispatches whose demangled name starts
-    with `prefix` (namespaces dropped), over the number of `per_call` ones."""
+def _kernel_kib(rows, prefix, per_call, calls):
+    """KiB per entry-point call over the first `calls` calls in dispatch order
+    (the main timed loop of the counter run; later dispatches of the same
+    kernels belong to other workloads): all dispatches whose demangled name
+    starts with `prefix` (namespaces dropped), up to and including the
+    `calls`-th dispatch named `per_call`, over `calls`."""
     def base(name):
         name = name.replace("(anonymous namespace)::", "")
         name = name[5:] if name.startswith("void ") else name
         return name.split("(")[0].split("<")[0].split("::")[-1].strip()
-    tot = sum(v for n, v in rows if base(n).startswith(prefix))
-    calls = sum(1 for n, _ in rows if base(n) == per_call)
-    if calls == 0:
-        raise SystemExit(f"no {per_call} dispatch in the counter file")
-    return tot / calls
+    tot, seen = 0.0, 0
+    for n, v in rows:
+        b = base(n)
+        if b.startswith(prefix):
+            tot += v
+        if b == per_call:
+            seen += 1
+            if seen == calls:
+                return tot / calls
+    raise SystemExit(f"fewer than {calls} {per_call} dispatches in the counter file")
 
 
 def record_traffic(folder):
@@ -122,9 +136,10 @@ def record_traffic(folder):
         rec = {}
     fetch_rows, write_rows = rows("tr_FETCH_SIZE"), rows("tr_WRITE_SIZE")
     cmd = "rocprofv3 --pmc {c} -f csv -d <out> -o run -- python -u <repo>/bench.py {a}"
+    calls = COUNTER_RUN_STEPS + COUNTER_RUN_WARMUP      # main-loop calls of the counter run
     for key, (prefix, per_call, sources) in TRAFFIC_KERNELS.items():
-        fk = _kernel_kib(fetch_rows, prefix, per_call)
-        wk = _kernel_kib(write_rows, prefix, per_call)
+        fk = _kernel_kib(fetch_rows, prefix, per_call, calls)
+        wk = _kernel_kib(write_rows, prefix, per_call, calls)
         rd, wr = fk * 1024.0 * fetch_f, wk * 1024.0 * write_f
         rec[key] = {
             "kernels": prefix + "*",
@@ -138,8 +153,10 @@ def record_traffic(folder):
             "hbm_read_bytes_per_launch": int(rd),
             "hbm_write_bytes_per_launch": int(wr),
             "hbm_bytes_per_launch": int(rd + wr),
+            "main_loop_calls_counted": calls,
             "commands": [cmd.format(c=c, a=a) for a in
-                         ("--no-cpu-baseline --steps 2 --warmup 1", "--copy-calibration")
+                         (f"--no-cpu-baseline --steps {COUNTER_RUN_STEPS} --warmup "
+                          f"{COUNTER_RUN_WARMUP}", "--copy-calibration")
                          for c in ("FETCH_SIZE", "WRITE_SIZE")],
         }
     with open(COUNTERS, "w") as f:

@@ -1,0 +1,158 @@
+"""Seeded random sweep of the HIP path against the CPU oracle.
+
+Each case draws its own shapes: prompt counts, ragged group sizes in
+[2, 64], score widths on and off the kernels' tile boundaries, padded row
+strides (NaN in the padding), fp32 and bf16 scores, binary / continuous /
+saturated rewards, continuation probabilities from near zero up to exactly 1,
+and design seeds and replicate offsets.  The bars are those of the parity
+tests: masks, logged rho and counts bit-exact; coefficients and fp32
+gradients within 1e-5 relative L2, bf16 gradients within 2e-3; exact zeros
+where the oracle's estimate is exactly zero; audit MSE, bias norm and
+per-replicate squared errors within 2e-3 relative, edge counts bit-exact.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_11368_amd as pair
+from tests.gpu_util import DEV, log, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+FP32_TOL = 1e-5
+BF16_TOL = 2e-3
+WIDTHS = (1, 2, 7, 31, 255, 1000, 1023, 1025, 2047, 2049, 4095, 4097, 6000)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    pair.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _bf16_bits(x):
+    """fp32 -> bf16 bit patterns (round to nearest even, torch on the host)."""
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.bfloat16) \
+        .view(torch.int16).numpy().view(np.uint16)
+
+
+def _case(rng, max_b, widths, bf16=None):
+    B = int(rng.integers(1, max_b + 1))
+    sizes = rng.integers(2, 65, size=B)
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    nv = int(offsets[-1])
+    D = int(rng.choice(widths))
+    if bf16 is None:
+        bf16 = bool(rng.integers(0, 2))
+    unit = 8 if bf16 else 4                          # 16-byte aligned rows
+    ld = (D + unit - 1) // unit * unit + int(rng.choice([0, unit, 3 * unit]))
+    rewards = np.empty(nv, dtype=np.float32)
+    p = np.empty(nv, dtype=np.float32)
+    for b in range(B):
+        o0, o1 = offsets[b], offsets[b + 1]
+        kind = rng.integers(0, 3)
+        if kind == 0:
+            rewards[o0:o1] = (rng.random(o1 - o0) < rng.random()).astype(np.float32)
+        elif kind == 1:
+            rewards[o0:o1] = rng.random(o1 - o0)
+        else:
+            rewards[o0:o1] = float(rng.integers(0, 2))     # saturated prompt
+        pmin = float(rng.choice([1e-3, 0.05, 0.3]))
+        p[o0:o1] = pmin + (1.0 - pmin) * rng.random(o1 - o0)
+        p[o0:o1][rng.random(o1 - o0) < 0.1] = 1.0
+    s = rng.standard_normal((nv, D)).astype(np.float32)
+    if bf16:
+        host = np.full((nv, ld), 0x7FC0, dtype=np.uint16)   # NaN padding
+        host[:, :D] = _bf16_bits(s)
+        dev = torch.from_numpy(host.view(np.int16)).to(DEV).view(torch.bfloat16)[:, :D]
+    else:
+        host = np.full((nv, ld), np.nan, dtype=np.float32)
+        host[:, :D] = s
+        dev = torch.from_numpy(host).to(DEV)[:, :D]
+    seed = int(rng.integers(0, 2**63))
+    rep0 = int(rng.integers(0, 1 << 20))
+    return dict(B=B, offsets=offsets, nv=nv, D=D, ld=ld, bf16=bf16, rewards=rewards, p=p,
+                host=host[:, :D], dev=dev, seed=seed, rep0=rep0, gmax=int(sizes.max()))
+
+
+@pytest.mark.parametrize("case_id", range(24))
+def test_random_gradient_chain(case_id):
+    rng = np.random.default_rng(7000 + case_id)
+    c = _case(rng, 24, WIDTHS)
+    B, nv, gmax, D = c["B"], c["nv"], c["gmax"], c["D"]
+    R = int(rng.integers(1, 4))
+    log(f"random chain {case_id}: B={B} nv={nv} gmax={gmax} D={D} ld={c['ld']} "
+        f"{'bf16' if c['bf16'] else 'fp32'} R={R} rep0={c['rep0']}")
+    off = torch.from_numpy(c["offsets"]).to(DEV)
+    rew = torch.from_numpy(c["rewards"]).to(DEV)
+    p = torch.from_numpy(c["p"]).to(DEV)
+
+    d = pair.design_inclusion(off, p, c["seed"], c["rep0"], R, gmax, nv=nv)
+    od = oracle.design_inclusion(c["offsets"], c["p"], c["seed"], c["rep0"], R, gmax)
+    torch.cuda.synchronize()
+    assert int(d["status"].item()) == 0
+    for key in ("mask", "pi", "edge_count", "completed"):
+        assert np.array_equal(d[key].cpu().numpy(), od[key]), key
+
+    r = R - 1                                        # the last replicate feeds the estimator
+    co = pair.edge_coeffs(off, rew, d["mask"][r], d["pi"], gmax, nv=nv)
+    want_c, ec = oracle.pair_coeffs(c["offsets"], c["rewards"], od["mask"][r], od["pi"])
+    got_c = co["coeff"].cpu().numpy()
+    assert int(co["status"].item()) == 0
+    assert rel_l2(got_c, want_c) <= FP32_TOL
+    assert np.all(got_c[want_c == 0.0] == 0.0)
+    assert np.array_equal(co["edge_count"].cpu().numpy(), ec)
+
+    # the one-launch draw + fold equals the two calls bitwise
+    coeff2 = torch.empty(nv, device=DEV)
+    mask2 = torch.empty(nv, dtype=torch.uint8, device=DEV)
+    pi2 = torch.empty((B, gmax, gmax), device=DEV)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    pair.pair_design_coeffs(B, nv, gmax, off, p, rew, c["seed"], c["rep0"] + r, coeff2, mask2, pi2,
+                            None, None, st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    assert torch.equal(mask2, d["mask"][r]) and torch.equal(pi2, d["pi"])
+    assert torch.equal(coeff2, co["coeff"])
+
+    est, _ = oracle.pair_grad(c["offsets"], c["host"], c["rewards"], od["mask"][r], od["pi"])
+    tol = BF16_TOL if c["bf16"] else FP32_TOL
+    g = pair.weighted_grad(off, c["dev"], co["coeff"], nv=nv)
+    out = g["out"].cpu().numpy()
+    assert int(g["status"].item()) == 0 and np.isfinite(out).all()
+    err = rel_l2(out, est)
+    log(f"  coeff rel L2 {rel_l2(got_c, want_c):.2e}, grad rel L2 {err:.2e}")
+    assert err <= tol
+    for b in range(B):
+        if not np.any(est[b]):
+            assert np.all(out[b] == 0.0), f"prompt {b} must be exactly zero"
+    gm = pair.weighted_grad(off, c["dev"], co["coeff"], nv=nv, reduce=True)["out"].cpu().numpy()
+    assert np.isfinite(gm).all() and rel_l2(gm, est.mean(axis=0)) <= tol
+
+
+@pytest.mark.parametrize("case_id", range(10))
+def test_random_audit(case_id):
+    rng = np.random.default_rng(9100 + case_id)
+    c = _case(rng, 5, (1, 33, 500, 2047, 2049, 3000), bf16=True)
+    R = int(rng.choice([1, 31, 32, 33, 100]))
+    B, nv, gmax = c["B"], c["nv"], c["gmax"]
+    log(f"random audit {case_id}: B={B} nv={nv} gmax={gmax} D={c['D']} ld={c['ld']} R={R} "
+        f"rep0={c['rep0']}")
+    off = torch.from_numpy(c["offsets"]).to(DEV)
+    got = pair.audit(off, c["dev"], torch.from_numpy(c["rewards"]).to(DEV),
+                     torch.from_numpy(c["p"]).to(DEV), c["seed"], c["rep0"], R, gmax, nv=nv)
+    torch.cuda.synchronize()
+    want = oracle.audit(c["offsets"], c["host"], c["rewards"], c["p"], c["seed"], c["rep0"], R,
+                        gmax=gmax)
+    assert int(got["status"].item()) == 0
+    assert np.array_equal(got["edge_count"].cpu().numpy(), want["edge_count"])
+    mse, bias = got["mse"].cpu().numpy(), got["bias_norm"].cpu().numpy()
+    e_err = rel_l2(got["rep_sqerr"].cpu().numpy(), want["rep_sqerr"])
+    m_err = np.max(np.abs(mse - want["mse"]) / np.maximum(want["mse"], 1e-300))
+    b_err = np.max(np.abs(bias - want["bias_norm"]) / np.maximum(want["bias_norm"], 1e-300))
+    log(f"  rep_sqerr rel L2 {e_err:.2e}, max mse rel {m_err:.2e}, max bias rel {b_err:.2e}")
+    assert e_err <= BF16_TOL and m_err <= BF16_TOL and b_err <= BF16_TOL
