@@ -46,6 +46,10 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "pair_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
+# A separately compiled copy of the oracle to load instead of liboracle.so.
+# Only the mutation test sets it, to run the pins against deliberately
+# broken copies of pair_oracle.c.
+_LIB_OVERRIDE = os.environ.get("PAIR_ORACLE_LIB")
 
 F32 = 0
 BF16 = 1
@@ -90,9 +94,12 @@ _lib = None
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-            build()
-        lib = ctypes.CDLL(_LIB)
+        if _LIB_OVERRIDE:
+            lib = ctypes.CDLL(_LIB_OVERRIDE)
+        else:
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build()
+            lib = ctypes.CDLL(_LIB)
         P = ctypes.c_void_p
         i64, i32, u64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
         lib.orc_philox4x64_10.argtypes = [P, P, P]

@@ -1,0 +1,138 @@
+"""Planted mistakes in the CPU oracle must fail its pins.
+
+Each case copies ``oracle/pair_oracle.c``, replaces one fragment with a
+plausible mistake, compiles the copy with the oracle's own flags, and runs the
+oracle pin tests against it in a fresh process (``PAIR_ORACLE_LIB`` points the
+oracle package at the copy).  The run must fail: a pin that lets the mistake
+through would let the same mistake through in the oracle itself.  The
+unmodified copy must pass, so the harness itself is checked too.
+
+The mistakes cover every part of the oracle: the edge term, the weights, the
+normaliser, the rho entry and the edge mask of the estimator (Eq. pair-ht);
+the half-edge split of the sequence advantages (Eq. pair-advantage); the
+Philox reading of the design draw (word, counter layout, key schedule), the
+induced-edge count and the logged rho block; bf16 widening; the audit's
+target, MSE and bias (App. D); the exact covariance trace of Prop. 1; and the
+conditional-Poisson inclusion probabilities.
+"""
+import concurrent.futures
+import os
+import subprocess
+import sys
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "pair_oracle.c")
+PINS = ["tests/test_oracle_pins.py", "tests/test_oracle_rules.py", "tests/test_oracle_exact.py",
+        "tests/test_oracle_cps.py"]
+CFLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-fPIC",
+          "-shared", "-w"]
+
+# (label, fragment of pair_oracle.c, replacement); the first occurrence is replaced.
+MUTATIONS = [
+    ("edge term without the 1/2",
+     "out[d] += 0.5 * (ri - rj) * (wi * si - wj * sj);",
+     "out[d] += (ri - rj) * (wi * si - wj * sj);"),
+    ("rho multiplied instead of divided",
+     "double w = 1.0 / rho;",
+     "double w = rho;"),
+    ("HT normaliser K_E instead of M",
+     "double N = M;\n    if (rule == ORC_RULE_RATIO_KE) N = (double)ke;\n    if (rule == ORC_RULE_SELFNORM) N = nsn;\n    for (int64_t d",
+     "double N = (double)ke;\n    if (rule == ORC_RULE_RATIO_KE) N = (double)ke;\n    if (rule == ORC_RULE_SELFNORM) N = nsn;\n    for (int64_t d"),
+    ("reward difference reversed",
+     "double ri = (double)rewards[o + i], rj = (double)rewards[o + j];",
+     "double ri = (double)rewards[o + j], rj = (double)rewards[o + i];"),
+    ("rho read from the diagonal",
+     "return (double)blk[lo * gmax + hi];",
+     "return (double)blk[lo * gmax + lo];"),
+    ("unobserved partner included",
+     "if (!(Ji && Jj)) continue; /* I_ij = 0: the edge is not observed */",
+     "if (!(Ji || Jj)) continue;"),
+    ("advantage: wrong sign on the second endpoint",
+     "coeff[o + j] -= 0.5 * dr * wj;",
+     "coeff[o + j] += 0.5 * dr * wj;"),
+    ("advantage: first endpoint without the 1/2",
+     "coeff[o + i] += 0.5 * dr * wi;",
+     "coeff[o + i] += dr * wi;"),
+    ("Philox: wrong output word",
+     "uint64_t u = w[i & 3] >> 32;",
+     "uint64_t u = w[(i + 1) & 3] >> 32;"),
+    ("Philox: replicate and prompt swapped in the counter",
+     "uint64_t ctr[4] = {(uint64_t)r, (uint64_t)b, (uint64_t)(i >> 2), 0};",
+     "uint64_t ctr[4] = {(uint64_t)b, (uint64_t)r, (uint64_t)(i >> 2), 0};"),
+    ("Philox: wrong Weyl constant",
+     "weyl1 = 0xBB67AE8584CAA73BULL",
+     "weyl1 = 0xBB67AE8584CAA73DULL"),
+    ("Philox: low half of the word",
+     "uint64_t u = w[i & 3] >> 32;",
+     "uint64_t u = w[i & 3] & 0xffffffffULL;"),
+    ("induced-edge count includes self pairs",
+     "/* brute-force count of induced edges */\n                for (int64_t j = i + 1; j < g; ++j)",
+     "/* brute-force count of induced edges */\n                for (int64_t j = i; j < g; ++j)"),
+    ("logged rho uses p_i twice",
+     "val = (float)((double)p[o + i] * (double)p[o + j]);",
+     "val = (float)((double)p[o + i] * (double)p[o + i]);"),
+    ("bf16 widened with the wrong shift",
+     "uint32_t bits = ((uint32_t)h) << 16;",
+     "uint32_t bits = ((uint32_t)h) << 15;"),
+    ("audit target weighted by 1/rho",
+     "s = ht_estimate_one(o, g, D, scores, dtype, ld, rewards, NULL, NULL, gmax, t, NULL);",
+     "s = ht_estimate_one(o, g, D, scores, dtype, ld, rewards, NULL, blk, gmax, t, NULL);"),
+    ("audit MSE over R - 1",
+     "if (mse) mse[b] = esum / (double)R;",
+     "if (mse) mse[b] = esum / (double)(R > 1 ? R - 1 : 1);"),
+    ("audit bias from the last replicate",
+     "double dev = gsum[d] / (double)R - t[d];",
+     "double dev = gr[d] - t[d];"),
+    ("exact audit: shared-vertex covariance dropped",
+     "tr += pi_ * pj * pk * (1.0 - pi_) * ip;",
+     "tr += 0.0 * ip;"),
+    ("exact audit: edge variance rho^2 instead of rho (1 - rho)",
+     "tr += rho * (1.0 - rho) * nn;",
+     "tr += rho * rho * nn;"),
+    ("conditional Poisson: joint probability without w_j",
+     "v = w[i] * w[j] * e[n - 2] / en;",
+     "v = w[i] * e[n - 2] / en;"),
+    ("conditional Poisson: first order without leaving unit i out",
+     "esp_excluding(w, g, n - 1, i, -1, e);",
+     "esp_excluding(w, g, n - 1, -1, -1, e);"),
+]
+
+
+def _build(src_text, folder, name):
+    c = os.path.join(folder, name + ".c")
+    so = os.path.join(folder, name + ".so")
+    with open(c, "w") as f:
+        f.write(src_text)
+    subprocess.run(["gcc", *CFLAGS, "-o", so, c, "-lm"], check=True, capture_output=True)
+    return so
+
+
+def _run_pins(so):
+    env = dict(os.environ, PAIR_ORACLE_LIB=so, OMP_NUM_THREADS="2")
+    res = subprocess.run([sys.executable, "-m", "pytest", *PINS, "-x", "-q", "-p", "no:cacheprovider",
+                          "-m", "not gpu", "-p", "no:xdist"],
+                         cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    return res.returncode, res.stdout[-2000:]
+
+
+def test_every_planted_mistake_fails_a_pin():
+    with open(SRC) as f:
+        src = f.read()
+    for label, old, new in MUTATIONS:
+        assert old in src, f"mutation site not found: {label}"
+    with tempfile.TemporaryDirectory() as tmp:
+        libs = {"unmodified": _build(src, tmp, "unmodified")}
+        for k, (label, old, new) in enumerate(MUTATIONS):
+            libs[label] = _build(src.replace(old, new, 1), tmp, f"mutant{k}")
+        with concurrent.futures.ThreadPoolExecutor(max_workers=4) as ex:
+            results = dict(zip(libs, ex.map(_run_pins, libs.values())))
+    rc, out = results.pop("unmodified")
+    assert rc == 0, "the unmodified copy must pass every pin:\n" + out
+    survivors = [label for label, (rc, _) in results.items() if rc == 0]
+    assert not survivors, f"planted mistakes no pin catches: {survivors}"
+    # every mutant failed a test (exit 1), not the harness (collection or usage error)
+    broken = {label: out for label, (rc, out) in results.items() if rc != 1}
+    assert not broken, f"mutant runs that did not end in a failing test: {list(broken)}"
