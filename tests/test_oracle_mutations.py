@@ -7,21 +7,25 @@ oracle package at the copy).  The run must fail: a pin that lets the mistake
 through would let the same mistake through in the oracle itself.  The
 unmodified copy must pass, so the harness itself is checked too.
 
+The same is done for the probability-design oracle, ``oracle/alloc.py``: a
+mutated copy is loaded in place of ``oracle.alloc`` in a fresh process and its
+pins are run.
+
 The mistakes cover every part of the oracle: the edge term, the weights, the
 normaliser, the rho entry and the edge mask of the estimator (Eq. pair-ht);
 the half-edge split of the sequence advantages (Eq. pair-advantage); the
 Philox reading of the design draw (word, counter layout, key schedule), the
 induced-edge count and the logged rho block; bf16 widening; the audit's
-target, MSE and bias (App. D); the exact covariance trace of Prop. 1; and the
-conditional-Poisson inclusion probabilities.
+target, MSE and bias (App. D); the exact covariance trace of Prop. 1; the
+conditional-Poisson inclusion probabilities; and the contrast graph's
+disagreement, edge proxy and vertex term, the design objective, its gradient
+and budget, and the pointwise and uniform comparison designs (Sec. 3.3-3.4).
 """
 import concurrent.futures
 import os
 import subprocess
 import sys
 import tempfile
-
-import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "pair_oracle.c")
@@ -134,5 +138,78 @@ def test_every_planted_mistake_fails_a_pin():
     survivors = [label for label, (rc, _) in results.items() if rc == 0]
     assert not survivors, f"planted mistakes no pin catches: {survivors}"
     # every mutant failed a test (exit 1), not the harness (collection or usage error)
+    broken = {label: out for label, (rc, out) in results.items() if rc != 1}
+    assert not broken, f"mutant runs that did not end in a failing test: {list(broken)}"
+
+
+ALLOC_SRC = os.path.join(ROOT, "oracle", "alloc.py")
+ALLOC_PINS = ["tests/test_oracle_alloc.py"]
+ALLOC_MUTATIONS = [
+    ("disagreement without the (1 - p_i) p_j term",
+     "d = p[:, None] * (1.0 - p[None, :]) + (1.0 - p[:, None]) * p[None, :]",
+     "d = p[:, None] * (1.0 - p[None, :]) + p[:, None] * p[None, :]"),
+    ("edge proxy over 2 instead of 4",
+     "a = a * (m[:, None] + m[None, :]) ** 2 / 4.0",
+     "a = a * (m[:, None] + m[None, :]) ** 2 / 2.0"),
+    ("vertex term without the diagonal correction",
+     "return np.sum(np.sqrt(a), axis=1) ** 2 - np.sum(a, axis=1)",
+     "return np.sum(np.sqrt(a), axis=1) ** 2"),
+    ("objective multiplies the vertex term by pi",
+     "return float(np.sum(a[iu] / (pi[iu[0]] * pi[iu[1]])) + np.sum(b / pi))",
+     "return float(np.sum(a[iu] / (pi[iu[0]] * pi[iu[1]])) + np.sum(b * pi))"),
+    ("solver gradient with the wrong sign",
+     "return -(iu * iu) * (sym @ iu + b) / f0",
+     "return (iu * iu) * (sym @ iu + b) / f0"),
+    ("budget row doubled",
+     'cons = {"type": "ineq", "fun": lambda u: 1.0 - float(cs @ u), "jac": lambda u: -cs}',
+     'cons = {"type": "ineq", "fun": lambda u: 2.0 - float(cs @ u), "jac": lambda u: -cs}'),
+    ("uniform design spends half the budget",
+     "pi = np.full(p.size, np.clip(budget / np.sum(c), pi_min, 1.0))",
+     "pi = np.full(p.size, np.clip(0.5 * budget / np.sum(c), pi_min, 1.0))"),
+    ("pointwise design with p instead of p (1 - p)",
+     "pi, ok = _solve(np.zeros_like(a), p * (1.0 - p), c, budget, pi_min)",
+     "pi, ok = _solve(np.zeros_like(a), p, c, budget, pi_min)"),
+]
+
+# Runs the allocation pins with a copy of alloc.py loaded as oracle.alloc.
+_ALLOC_BOOT = """
+import importlib.util, sys
+import pytest
+import oracle
+spec = importlib.util.spec_from_file_location("oracle.alloc", sys.argv[1])
+mod = importlib.util.module_from_spec(spec)
+spec.loader.exec_module(mod)
+sys.modules["oracle.alloc"] = mod
+oracle.alloc = mod
+sys.exit(pytest.main(sys.argv[2:]))
+"""
+
+
+def _run_alloc_pins(path):
+    env = dict(os.environ, OMP_NUM_THREADS="2")
+    res = subprocess.run([sys.executable, "-c", _ALLOC_BOOT, path, *ALLOC_PINS, "-x", "-q",
+                          "-p", "no:cacheprovider", "-m", "not gpu", "-p", "no:xdist"],
+                         cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    return res.returncode, res.stdout[-2000:]
+
+
+def test_every_planted_allocation_mistake_fails_a_pin():
+    with open(ALLOC_SRC) as f:
+        src = f.read()
+    for label, old, new in ALLOC_MUTATIONS:
+        assert old in src, f"mutation site not found: {label}"
+    with tempfile.TemporaryDirectory() as tmp:
+        paths = {}
+        for k, (label, old, new) in enumerate([("unmodified", "", "")] + ALLOC_MUTATIONS):
+            path = os.path.join(tmp, f"alloc_{k}.py")
+            with open(path, "w") as f:
+                f.write(src.replace(old, new, 1) if old else src)
+            paths[label] = path
+        with concurrent.futures.ThreadPoolExecutor(max_workers=4) as ex:
+            results = dict(zip(paths, ex.map(_run_alloc_pins, paths.values())))
+    rc, out = results.pop("unmodified")
+    assert rc == 0, "the unmodified copy must pass every pin:\n" + out
+    survivors = [label for label, (rc, _) in results.items() if rc == 0]
+    assert not survivors, f"planted mistakes no pin catches: {survivors}"
     broken = {label: out for label, (rc, out) in results.items() if rc != 1}
     assert not broken, f"mutant runs that did not end in a failing test: {list(broken)}"
