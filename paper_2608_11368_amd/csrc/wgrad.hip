@@ -9,10 +9,13 @@
 // contiguous run (full cache lines for the fp32 output).
 // The prompt's nonzero coefficients are found with a
 // ballot (zero rows are never read: an uncompleted rollout has no score), the
-// row indices and coefficients become wave-uniform scalars, and up to 8 rows
-// are loaded back-to-back before any FMA so each lane keeps up to 256 bytes
+// row indices and coefficients become wave-uniform scalars, and up to 12 rows
+// are loaded back-to-back before any FMA so each lane keeps up to 384 bytes
 // in flight.  Rows are summed in ascending order, so results are
-// deterministic.
+// deterministic.  Tiles that lie wholly inside the row are one launch of a
+// kernel with no tail handling (fewer live registers, three waves per SIMD);
+// when D is not a multiple of the tile, the last tile of every prompt is a
+// second launch of the variant that guards each column.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -21,7 +24,7 @@ namespace pair {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kBatch = 8;    // rows loaded back to back per batch
+constexpr int kBatch = 12;   // rows loaded back to back per batch
 constexpr int kPieceCols = 4;  // columns per piece: one 16-byte fp32 output store
 
 // A lane owns kPieces pieces of 4 columns per tile; piece p of lane t covers
@@ -66,11 +69,16 @@ struct PieceTraits<false> {
   }
 };
 
-template <bool BF16>
+// TAIL = false: every tile of the launch lies wholly inside [0, D).
+// TAIL = true: the launch holds the last tile of each prompt, which may end
+// inside a piece; columns past D are neither read nor written.
+// Workgroup x of the launch covers prompt x / tiles_per_prompt and tile
+// tile0 + x % tiles_per_prompt.
+template <bool BF16, bool TAIL>
 __global__ __launch_bounds__(kThreads) void wgrad_kernel(
     int64_t B, int64_t nv, const int64_t* __restrict__ offsets,
     const unsigned char* __restrict__ scores, int64_t row_bytes, const float* __restrict__ coeff,
-    float* __restrict__ out, int64_t D, int64_t tiles_per_prompt, int vec_out,
+    float* __restrict__ out, int64_t D, int64_t tiles_per_prompt, int64_t tile0, int vec_out,
     int32_t* d_status) {
   using T = PieceTraits<BF16>;
   constexpr int NP = T::kPieces;
@@ -78,7 +86,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_kernel(
   constexpr int64_t kTileCols = kSpan * NP;
 
   const int64_t b = blockIdx.x / tiles_per_prompt;
-  const int64_t tile = blockIdx.x - b * tiles_per_prompt;
+  const int64_t tile = tile0 + (blockIdx.x - b * tiles_per_prompt);
   if (b >= B) return;
   const int lane = threadIdx.x & (kWave - 1);
   int64_t o0, g;
@@ -93,8 +101,8 @@ __global__ __launch_bounds__(kThreads) void wgrad_kernel(
 #pragma unroll
   for (int q = 0; q < NP; ++q) {
     c0[q] = tile * kTileCols + q * kSpan + (int64_t)threadIdx.x * kPieceCols;
-    full[q] = c0[q] + kPieceCols <= D;
-    part[q] = !full[q] && c0[q] < D;
+    full[q] = !TAIL || c0[q] + kPieceCols <= D;
+    part[q] = TAIL && !full[q] && c0[q] < D;
   }
 
   float acc[NP][kPieceCols];
@@ -137,7 +145,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_kernel(
           if (s < n && full[q]) T::fma(acc[q], cs[s], v[s][q]);
 #pragma unroll
       for (int q = 0; q < NP; ++q) {
-        if (part[q]) {   // the ragged tail of the last tile
+        if (TAIL && part[q]) {   // the ragged tail of the last tile
           for (int s = 0; s < n; ++s) {
             const unsigned char* row = base + roff[s];
             for (int e = 0; e < kPieceCols; ++e)
@@ -153,7 +161,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_kernel(
   for (int q = 0; q < NP; ++q) {
     if (full[q] && vec_out) {
       store_nt16(orow + c0[q], acc[q][0], acc[q][1], acc[q][2], acc[q][3]);
-    } else if (full[q] || part[q]) {
+    } else if (full[q] || (TAIL && part[q])) {
       for (int e = 0; e < kPieceCols; ++e)
         if (c0[q] + e < D) orow[c0[q] + e] = acc[q][e];
     }
@@ -261,16 +269,28 @@ int launch_wgrad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D, const
     return hipGetLastError() == hipSuccess ? PAIR_OK : PAIR_EHIP;
   }
   const int64_t tile = (int64_t)kThreads * kPieceCols * (bf16 ? 4 : 2);
-  const int64_t tiles = (D + tile - 1) / tile;
-  const int64_t grid = B * tiles;
-  if (grid > 0x7fffffffLL) return PAIR_ERANGE;
-  if (bf16) {
-    hipLaunchKernelGGL(wgrad_kernel<true>, dim3((unsigned)grid), dim3(kThreads), 0, stream, B, nv,
-                       offsets, s, row_bytes, coeff, out, D, tiles, vec_out, d_status);
-  } else {
-    hipLaunchKernelGGL(wgrad_kernel<false>, dim3((unsigned)grid), dim3(kThreads), 0, stream, B,
-                       nv, offsets, s, row_bytes, coeff, out, D, tiles, vec_out, d_status);
+  const int64_t full_tiles = D / tile;                 // tiles wholly inside [0, D)
+  const bool tail = full_tiles * tile < D;
+  if (B * full_tiles > 0x7fffffffLL) return PAIR_ERANGE;
+#define PAIR_WGRAD(BF, TL, GRID, TPP, T0)                                                         \
+  hipLaunchKernelGGL((wgrad_kernel<BF, TL>), dim3((unsigned)(GRID)), dim3(kThreads), 0, stream, B, \
+                     nv, offsets, s, row_bytes, coeff, out, D, TPP, T0, vec_out, d_status)
+  if (full_tiles > 0) {
+    if (bf16) {
+      PAIR_WGRAD(true, false, B * full_tiles, full_tiles, 0);
+    } else {
+      PAIR_WGRAD(false, false, B * full_tiles, full_tiles, 0);
+    }
+    if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
   }
+  if (tail) {
+    if (bf16) {
+      PAIR_WGRAD(true, true, B, 1, full_tiles);
+    } else {
+      PAIR_WGRAD(false, true, B, 1, full_tiles);
+    }
+  }
+#undef PAIR_WGRAD
   return hipGetLastError() == hipSuccess ? PAIR_OK : PAIR_EHIP;
 }
 
