@@ -19,12 +19,18 @@
 //                    v_mfma_f32_16x16x32_bf16 the A fragment (rows of S) and
 //                    the B fragment (columns of S^T) of a lane are the same
 //                    registers, so K_partial = sum_k S[m][k] S[n][k] needs one
-//                    16-byte load per row block per lane and step.  Lane l
-//                    loads row 16 q + l % 16, columns c + 32 t + 8 (l / 16)
-//                    .. + 7 for steps t = 0..3 (64 contiguous bytes per row and
-//                    instruction group); only the upper triangle of row blocks
-//                    is multiplied.  The four waves are added in fixed order in
-//                    LDS and the slice's fp32 partial Gram is written out.
+//                    16-byte fragment per row block per lane and step; only
+//                    the upper triangle of row blocks is multiplied.  The
+//                    slice is streamed in chunks of 512 columns: every wave
+//                    loads whole 1 KB runs of its rows (coalesced), the chunk
+//                    is staged in LDS (two buffers, rows skewed by 16 bytes),
+//                    and lane l then reads the fragment of row 16 q + l % 16,
+//                    columns 128 w + 32 t + 8 (l / 16) .. + 7 of wave w's
+//                    part, step t = 0..3.  The loads of the next chunks (two
+//                    ahead for G <= 16, one ahead above) are in flight while
+//                    a chunk is multiplied.  The four waves are added in
+//                    fixed order in LDS and the slice's fp32 partial Gram is
+//                    written out.
 //  2. exact_final_kernel  workgroup per prompt: K in fp64 (slices summed in
 //                    order), the rule's coefficients, beta^T K beta and the
 //                    covariance trace with a fixed-order reduction.
@@ -40,15 +46,17 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kGramThreads = 256;
 constexpr int kGramWaves = kGramThreads / kWave;
-constexpr int kStepCols = 128;        // columns per wave step (4 matrix instructions)
+constexpr int kStepCols = 128;                       // columns per wave step (4 matrix instructions)
+constexpr int kChunkCols = kGramWaves * kStepCols;   // columns staged per chunk
+constexpr int kChunkStride = kChunkCols + 8;         // LDS row stride (bf16), 16-byte skew
 constexpr int kFinalThreads = 256;
 
-inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 struct ExactLayout {
   int ks, kp;
   int64_t nsl;     // column slices per prompt
-  int64_t slice;   // columns per slice (multiple of kStepCols)
+  int64_t slice;   // columns per slice (multiple of kChunkCols)
   size_t total;
 };
 
@@ -56,12 +64,12 @@ ExactLayout exact_layout(int64_t B, int32_t gmax, int64_t D) {
   ExactLayout L;
   L.ks = (gmax + 15) / 16;
   L.kp = 16 * L.ks;
-  // At least ~2048 workgroups over the batch, slices of at least 1024 columns.
-  int64_t nsl = ceil_div(2048, B);
-  const int64_t max_sl = ceil_div(D, 1024);
+  // About 8192 workgroups over the batch, slices of at least one chunk.
+  int64_t nsl = ceil_div(8192, B);
+  const int64_t max_sl = ceil_div(D, kChunkCols);
   if (nsl > max_sl) nsl = max_sl;
   if (nsl < 1) nsl = 1;
-  L.slice = ceil_div(ceil_div(D, nsl), kStepCols) * kStepCols;
+  L.slice = ceil_div(ceil_div(D, nsl), kChunkCols) * kChunkCols;
   L.nsl = ceil_div(D, L.slice);
   L.total = (size_t)B * L.nsl * L.kp * L.kp * sizeof(float);
   return L;
@@ -73,7 +81,12 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(
     const uint16_t* __restrict__ scores, int64_t ld, int64_t nsl, int64_t slice,
     float* __restrict__ part) {
   constexpr int KP = 16 * KS;
-  __shared__ float red[KP * KP];
+  constexpr int kAhead = KS == 1 ? 2 : 1;        // chunks whose loads are in flight
+  constexpr int kRows = KP / kGramWaves;          // rows each wave loads per chunk
+  constexpr int kBufElems = KP * kChunkStride;    // one staged chunk
+  static_assert(2 * kBufElems * 2 >= KP * KP * 4, "the reduction reuses the staging buffers");
+  __shared__ __align__(16) uint16_t stage[2 * kBufElems];
+  float* red = reinterpret_cast<float*>(stage);   // wave sums, after the last chunk
   const int64_t b = blockIdx.x / nsl;
   const int64_t sl = blockIdx.x - b * nsl;
   int64_t o0, g;
@@ -84,48 +97,81 @@ __global__ __launch_bounds__(kGramThreads) void gram_kernel(
   const int rsub = lane & 15;
   const int kgrp = lane >> 4;
 
+  const int64_t c_lo = sl * slice;
+  const int64_t c_hi = c_lo + slice < D ? c_lo + slice : D;
+  const int nchunks = (int)ceil_div(c_hi - c_lo, kChunkCols);
+
+  // Chunk k, row wave + 4 i, columns c_lo + 512 k + 8 lane .. + 7 (zero past
+  // the slice or the prompt's rows).
+  auto gload = [&](int k, uint4 (&r)[kRows]) {
+#pragma unroll
+    for (int i = 0; i < kRows; ++i) {
+      const int row = wave + kGramWaves * i;
+      const int64_t col = c_lo + (int64_t)k * kChunkCols + 8 * lane;
+      uint4 v = make_uint4(0u, 0u, 0u, 0u);
+      if (row < g) {
+        const uint16_t* src = scores + (o0 + row) * ld + col;
+        if (col + 8 <= c_hi) {
+          v = load_nt16(src);
+        } else if (col < c_hi) {
+          uint16_t h[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) h[e] = (col + e < c_hi) ? src[e] : (uint16_t)0;
+          v.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+          v.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+          v.z = (uint32_t)h[4] | ((uint32_t)h[5] << 16);
+          v.w = (uint32_t)h[6] | ((uint32_t)h[7] << 16);
+        }
+      }
+      r[i] = v;
+    }
+  };
+  auto lstore = [&](int k, const uint4 (&r)[kRows]) {
+    uint16_t* dst = stage + (k & 1) * kBufElems;
+#pragma unroll
+    for (int i = 0; i < kRows; ++i)
+      *reinterpret_cast<uint4*>(dst + (wave + kGramWaves * i) * kChunkStride + 8 * lane) = r[i];
+  };
+
   f32x4_t acc[KS][KS];
 #pragma unroll
   for (int a = 0; a < KS; ++a)
 #pragma unroll
     for (int c = 0; c < KS; ++c) acc[a][c] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
-  const int64_t c_lo = sl * slice;
-  const int64_t c_hi = c_lo + slice < D ? c_lo + slice : D;
-  for (int64_t c = c_lo + (int64_t)wave * kStepCols; c < c_hi; c += kGramWaves * kStepCols) {
-    bf16x8_t fr[KS][4];
+  // Register slot u % kAhead holds chunk u until it is staged in LDS.
+  uint4 st[kAhead][kRows];
 #pragma unroll
-    for (int q = 0; q < KS; ++q) {
-      const int row = 16 * q + rsub;
-      const uint16_t* src = scores + (o0 + row) * ld;
+  for (int u = 0; u < kAhead; ++u)
+    if (u < nchunks) gload(u, st[u]);
+  lstore(0, st[0]);
+  __syncthreads();
+  for (int k0 = 0; k0 < nchunks; k0 += kAhead) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int64_t col = c + 32 * t + 8 * kgrp;
-        uint4 v = make_uint4(0u, 0u, 0u, 0u);
-        if (row < g) {
-          if (col + 8 <= c_hi) {
-            v = load_nt16(src + col);
-          } else if (col < c_hi) {
-            uint16_t h[8];
+    for (int u = 0; u < kAhead; ++u) {
+      const int k = k0 + u;
+      if (k < nchunks) {
+        // slot u held chunk k, already staged: refill it with chunk k + kAhead
+        if (k + kAhead < nchunks) gload(k + kAhead, st[u]);
+        const uint16_t* cur = stage + (k & 1) * kBufElems;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) h[e] = (col + e < c_hi) ? src[col + e] : (uint16_t)0;
-            v.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
-            v.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
-            v.z = (uint32_t)h[4] | ((uint32_t)h[5] << 16);
-            v.w = (uint32_t)h[6] | ((uint32_t)h[7] << 16);
-          }
+        for (int t = 0; t < 4; ++t) {
+          bf16x8_t fr[KS];
+#pragma unroll
+          for (int q = 0; q < KS; ++q)
+            fr[q] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(
+                cur + (16 * q + rsub) * kChunkStride + kStepCols * wave + 32 * t + 8 * kgrp));
+#pragma unroll
+          for (int a = 0; a < KS; ++a)
+#pragma unroll
+            for (int c2 = a; c2 < KS; ++c2)
+              acc[a][c2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fr[a], fr[c2], acc[a][c2],
+                                                                    0, 0, 0);
         }
-        fr[q][t] = __builtin_bit_cast(bf16x8_t, v);
+        if (k + 1 < nchunks) lstore(k + 1, st[(u + 1) % kAhead]);
+        __syncthreads();
       }
     }
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int a = 0; a < KS; ++a)
-#pragma unroll
-        for (int c2 = a; c2 < KS; ++c2)
-          acc[a][c2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fr[a][t], fr[c2][t], acc[a][c2],
-                                                                0, 0, 0);
   }
 
   // Accumulator v of tile (a, c2): row 16 a + 4 (l / 16) + v, column

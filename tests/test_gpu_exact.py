@@ -45,7 +45,8 @@ def _check(got, want, label):
 
 @pytest.mark.parametrize("name,rule,wmax", LINEAR)
 @pytest.mark.parametrize("wname,B,D,G", [("audit", 6, 4096 + 40, None), ("ragged", 12, 777, None),
-                                         ("audit", 4, 3000, 20), ("audit", 3, 1500, 40)])
+                                         ("audit", 4, 3000, 20), ("audit", 3, 1500, 40),
+                                         ("audit", 3, 100, None), ("ragged", 5, 1, None)])
 def test_exact_audit_vs_oracle(name, rule, wmax, wname, B, D, G):
     w = wl.WORKLOADS[wname].replace(B=B, D=D)
     if G is not None:
@@ -82,6 +83,33 @@ def test_gram_output_matches_host_product():
         g = hi - lo
         err = np.max(np.abs(gram[b, :g, :g] - K)) / np.max(np.abs(K))
         assert err <= 1e-5, (b, err)
+
+
+@pytest.mark.parametrize("B,G,D", [(64, 16, 140001), (50, 40, 90001)])
+def test_gram_multi_chunk_slices(B, G, D):
+    """Shapes whose column slices hold several 512-column chunks, so the
+    staged loads run ahead of the multiplication (two chunks ahead for
+    G <= 16, one above), with a ragged last chunk; the Gram blocks against
+    an fp64 host product of the same bf16 rows."""
+    w = wl.WORKLOADS["audit"].replace(B=B, G=G, D=D)
+    meta = wl.host_meta(w)
+    log(f"gram multi-chunk B={B} G={G} D={D}")
+    dm = upload_meta(meta)
+    sd = wl.device_scores(w, meta.nv, DEV, ld=(D + 7) // 8 * 8)[:, :D]   # 16-byte aligned rows
+    got = pair.audit_exact(dm["offsets"], sd, dm["rewards"], dm["p"], meta.gmax, want_gram=True,
+                           nv=meta.nv)
+    torch.cuda.synchronize()
+    assert int(got["status"].item()) == 0
+    gram = got["gram"].cpu().numpy()
+    worst = 0.0
+    for b in range(meta.B):
+        lo, hi = meta.offsets[b], meta.offsets[b + 1]
+        sf = sd[lo:hi].float().cpu().numpy().astype(np.float64)
+        K = sf @ sf.T
+        err = np.max(np.abs(gram[b, : hi - lo, : hi - lo] - K)) / np.max(np.abs(K))
+        worst = max(worst, err)
+    log(f"  max rel err {worst:.2e}")
+    assert worst <= 1e-5
 
 
 def test_exact_audit_rejects_ratio_rules():
