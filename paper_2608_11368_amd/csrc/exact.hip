@@ -237,8 +237,17 @@ __global__ __launch_bounds__(kFinalThreads) void exact_final_kernel(
     double k = 0.0;
     const int i = idx / KP, j = idx - i * KP;
     if (i < gi && j < gi) {
+      // slice partials added in slice order; loaded eight at a time
       const float* src = part + b * nsl * (int64_t)KP * KP + idx;
-      for (int64_t s = 0; s < nsl; ++s) k += (double)src[s * (int64_t)KP * KP];
+      int64_t s = 0;
+      for (; s + 8 <= nsl; s += 8) {
+        float v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = src[(s + q) * (int64_t)KP * KP];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) k += (double)v[q];
+      }
+      for (; s < nsl; ++s) k += (double)src[s * (int64_t)KP * KP];
       if (!isfinite(k)) nonfinite = true;
       if (gram != nullptr) gram[(b * gmax + i) * (int64_t)gmax + j] = k;
     }
