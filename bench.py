@@ -224,6 +224,83 @@ def cpu_baseline(meta, w, scores_dev, meta_a, wa, scores_a_dev, budget_s=24.0):
     }
 
 
+def _grow(fn, target_s, n0, n_max):
+    """Run fn(n) with n doubling (or more) until it takes target_s or n reaches
+    n_max; returns (n, seconds) of the last run."""
+    n = n0
+    while True:
+        t0 = time.perf_counter()
+        fn(n)
+        dt = time.perf_counter() - t0
+        if dt >= target_s or n >= n_max:
+            return n, dt
+        n = min(n_max, n * max(2, int(target_s / max(dt, 1e-3))))
+
+
+def cpu_next_rows(wl, meta_a, wa, scores_a_dev, target_s=2.0):
+    """The CPU oracle on bounded samples of the widened rows' workloads: the
+    estimator variants (audit replay per edge-weight rule), the exact audit,
+    the probability design and the fixed-size design fit.  Returns one dict
+    per row, to sit beside that row's GPU timing."""
+    import numpy as np
+
+    import oracle
+    from oracle import alloc as oalloc
+    from tests.gpu_util import scores_to_host
+
+    cores = oracle.num_threads()
+    o0, o1 = meta_a.offsets[0], meta_a.offsets[1]
+    sa0 = scores_to_host(scores_a_dev[o0:o1])
+    out = {}
+
+    def variants(reps):
+        for rule in range(len(RULE_NAMES)):
+            oracle.audit(np.array([0, o1 - o0]), sa0, meta_a.rewards[o0:o1], meta_a.p[o0:o1],
+                         wa.design_seed, 0, reps, prompt_id=[0], want_reps=False, rule=rule,
+                         wmax=10.0 if RULE_NAMES[rule] == "clipped" else 0.0)
+    n, dt = _grow(variants, target_s, 4, wa.R)
+    out["variants"] = {"value": round(n * len(RULE_NAMES) / dt, 1), "unit": "replicate-estimates/s",
+                       "cores": cores, "kind": "oracle",
+                       "sample": f"audit workload prompt 0, {n} replicates under each of the "
+                                 f"{len(RULE_NAMES)} rules: {dt:.2f} s"}
+
+    def exact(k):
+        lo, hi = meta_a.offsets[0], meta_a.offsets[k]
+        oracle.audit_exact(meta_a.offsets[:k + 1] - lo, scores_to_host(scores_a_dev[lo:hi]),
+                           meta_a.rewards[lo:hi], meta_a.p[lo:hi], gmax=meta_a.gmax)
+    n, dt = _grow(exact, target_s, 1, meta_a.B)
+    out["exact_audit"] = {"value": round(n / dt, 1), "unit": "prompts/s", "cores": cores,
+                          "kind": "oracle",
+                          "sample": f"first {n} prompts of the audit workload: {dt:.2f} s"}
+
+    wr = wl.WORKLOADS["ragged"]
+    mr = wl.host_meta(wr)
+    inp = wl.alloc_inputs(wr, mr.offsets)
+
+    def design(k):
+        oalloc.solve_batch(mr.offsets[:k + 1], inp.p_hat, inp.c_hat, inp.budget[:k], 0.08,
+                           oalloc.PAIR)
+    n, dt = _grow(design, target_s, 1, mr.B)
+    out["design_alloc"] = {"value": round(n / dt, 1), "unit": "prompts/s", "cores": 1,
+                           "kind": "oracle",
+                           "sample": f"first {n} prompts of the ragged structure, graph-coupled "
+                                     f"design (SLSQP, one thread): {dt:.2f} s"}
+
+    tg = wl.cps_targets(mr.offsets)
+
+    def cps(k):
+        for b in range(k):
+            lo, hi = mr.offsets[b], mr.offsets[b + 1]
+            t = tg[lo:hi].astype(np.float64)
+            oracle.cps_fit(t, int(round(float(t.sum()))))
+    n, dt = _grow(cps, target_s, 1, mr.B)
+    out["fixed_size_design"] = {"value": round(n / dt, 1), "unit": "prompts/s", "cores": 1,
+                                "kind": "oracle",
+                                "sample": f"fit of the first {n} prompts of the ragged structure "
+                                          f"(one thread): {dt:.2f} s"}
+    return out
+
+
 def _cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -658,6 +735,9 @@ def main():
     if not args.no_cpu_baseline:
         _log("[bench] timing the CPU oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(meta, w, scores, meta_a, wa, scores_a)
+        _log("[bench] timing the CPU oracle of the widened rows")
+        for key, rec in cpu_next_rows(wl, meta_a, wa, scores_a).items():
+            result[key]["cpu_oracle"] = rec
     print(json.dumps(result), flush=True)
 
 
