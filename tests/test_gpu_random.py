@@ -4,8 +4,10 @@ Each case draws its own shapes: prompt counts, ragged group sizes in
 [2, 64], score widths on and off the kernels' tile boundaries, padded row
 strides (NaN in the padding), fp32 and bf16 scores, binary / continuous /
 saturated rewards, continuation probabilities from near zero up to exactly 1,
-and design seeds and replicate offsets.  The bars are those of the parity
-tests: masks, logged rho and counts bit-exact; coefficients and fp32
+and design seeds and replicate offsets.  The sweep covers the HT chain and
+audit, every edge-weight rule (coefficients, ESS, maximum weight, gradient,
+audit replay) and the exact audit of the linear rules.  The bars are those of
+the parity tests: masks, logged rho and counts bit-exact; coefficients and fp32
 gradients within 1e-5 relative L2, bf16 gradients within 2e-3; exact zeros
 where the oracle's estimate is exactly zero; audit MSE, bias norm and
 per-replicate squared errors within 2e-3 relative, edge counts bit-exact.
@@ -156,3 +158,105 @@ def test_random_audit(case_id):
     b_err = np.max(np.abs(bias - want["bias_norm"]) / np.maximum(want["bias_norm"], 1e-300))
     log(f"  rep_sqerr rel L2 {e_err:.2e}, max mse rel {m_err:.2e}, max bias rel {b_err:.2e}")
     assert e_err <= BF16_TOL and m_err <= BF16_TOL and b_err <= BF16_TOL
+
+
+RULES = [pair.RULE_HT, pair.RULE_UNWEIGHTED, pair.RULE_RATIO_KE, pair.RULE_CLIPPED,
+         pair.RULE_SELFNORM, pair.RULE_MARGINAL]
+LINEAR_RULES = [pair.RULE_HT, pair.RULE_UNWEIGHTED, pair.RULE_CLIPPED, pair.RULE_MARGINAL]
+
+
+def _rel_max(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.max(np.abs(a - b) / np.maximum(np.abs(b), 1e-30))) if a.size else 0.0
+
+
+def _wmax(rng, rule):
+    return float(rng.choice([2.0, 10.0, 50.0])) if rule == pair.RULE_CLIPPED else 0.0
+
+
+@pytest.mark.parametrize("case_id", range(12))
+def test_random_rule_coefficients_and_gradient(case_id):
+    rng = np.random.default_rng(9500 + case_id)
+    c = _case(rng, 16, WIDTHS)
+    rule = RULES[case_id % len(RULES)]
+    wmax = _wmax(rng, rule)
+    B, nv, gmax = c["B"], c["nv"], c["gmax"]
+    log(f"random rule {rule} (wmax {wmax}) case {case_id}: B={B} nv={nv} gmax={gmax} D={c['D']} "
+        f"{'bf16' if c['bf16'] else 'fp32'}")
+    off = torch.from_numpy(c["offsets"]).to(DEV)
+    rew = torch.from_numpy(c["rewards"]).to(DEV)
+    d = pair.design_inclusion(off, torch.from_numpy(c["p"]).to(DEV), c["seed"], c["rep0"], 1, gmax,
+                              nv=nv)
+    co = pair.edge_coeffs(off, rew, d["mask"][0], d["pi"], gmax, nv=nv, rule=rule, wmax=wmax)
+    g = pair.weighted_grad(off, c["dev"], co["coeff"], nv=nv)
+    torch.cuda.synchronize()
+    assert int(co["status"].item()) == 0
+    od = oracle.design_inclusion(c["offsets"], c["p"], c["seed"], c["rep0"], 1, gmax)
+    assert np.array_equal(d["mask"].cpu().numpy(), od["mask"])
+    oc = oracle.pair_coeffs_rule(c["offsets"], c["rewards"], mask=od["mask"][0], pi=od["pi"],
+                                 rule=rule, wmax=wmax)
+    coeff = co["coeff"].cpu().numpy()
+    assert rel_l2(coeff, oc["coeff"]) <= FP32_TOL
+    if rule != pair.RULE_MARGINAL:   # the marginal-only fold is not centred, so not antisymmetric
+        assert np.all(coeff[oc["coeff"] == 0.0] == 0.0)
+    assert np.array_equal(co["edge_count"].cpu().numpy(), oc["edge_count"])
+    assert _rel_max(co["ess"].cpu().numpy(), oc["ess"]) <= 1e-5
+    assert _rel_max(co["max_weight"].cpu().numpy(), oc["max_weight"]) <= 1e-6
+    og = oracle.pair_grad_rule(c["offsets"], c["host"], c["rewards"], mask=od["mask"][0],
+                               pi=od["pi"], rule=rule, wmax=wmax)
+    err = rel_l2(g["out"].cpu().numpy(), og["out"])
+    log(f"  coeff rel L2 {rel_l2(coeff, oc['coeff']):.2e}, grad rel L2 {err:.2e}")
+    assert err <= (BF16_TOL if c["bf16"] else FP32_TOL)
+
+
+@pytest.mark.parametrize("case_id", range(6))
+def test_random_rule_audit(case_id):
+    rng = np.random.default_rng(9700 + case_id)
+    c = _case(rng, 4, (33, 500, 2049), bf16=True)
+    rule = RULES[case_id % len(RULES)]
+    wmax = _wmax(rng, rule)
+    R = int(rng.choice([31, 64]))
+    B, nv, gmax = c["B"], c["nv"], c["gmax"]
+    log(f"random rule audit {rule} case {case_id}: B={B} gmax={gmax} D={c['D']} R={R}")
+    off = torch.from_numpy(c["offsets"]).to(DEV)
+    got = pair.audit(off, c["dev"], torch.from_numpy(c["rewards"]).to(DEV),
+                     torch.from_numpy(c["p"]).to(DEV), c["seed"], c["rep0"], R, gmax, nv=nv,
+                     rule=rule, wmax=wmax)
+    torch.cuda.synchronize()
+    want = oracle.audit(c["offsets"], c["host"], c["rewards"], c["p"], c["seed"], c["rep0"], R,
+                        gmax=gmax, rule=rule, wmax=wmax)
+    assert int(got["status"].item()) == 0
+    assert np.array_equal(got["edge_count"].cpu().numpy(), want["edge_count"])
+    mse, bias = got["mse"].cpu().numpy(), got["bias_norm"].cpu().numpy()
+    e_err = rel_l2(got["rep_sqerr"].cpu().numpy(), want["rep_sqerr"])
+    m_err = np.max(np.abs(mse - want["mse"]) / np.maximum(want["mse"], 1e-300))
+    b_err = np.max(np.abs(bias - want["bias_norm"]) / np.maximum(want["bias_norm"], 1e-300))
+    log(f"  rep_sqerr rel L2 {e_err:.2e}, max mse rel {m_err:.2e}, max bias rel {b_err:.2e}")
+    assert e_err <= BF16_TOL and m_err <= BF16_TOL and b_err <= BF16_TOL
+
+
+@pytest.mark.parametrize("case_id", range(8))
+def test_random_exact_audit(case_id):
+    rng = np.random.default_rng(9900 + case_id)
+    c = _case(rng, 6, (1, 100, 513, 2049, 5000), bf16=True)
+    rule = LINEAR_RULES[case_id % len(LINEAR_RULES)]
+    wmax = _wmax(rng, rule)
+    B, nv, gmax = c["B"], c["nv"], c["gmax"]
+    log(f"random exact audit {rule} case {case_id}: B={B} gmax={gmax} D={c['D']} ld={c['ld']}")
+    off = torch.from_numpy(c["offsets"]).to(DEV)
+    got = pair.audit_exact(off, c["dev"], torch.from_numpy(c["rewards"]).to(DEV),
+                           torch.from_numpy(c["p"]).to(DEV), gmax, rule=rule, wmax=wmax, nv=nv)
+    torch.cuda.synchronize()
+    want = oracle.audit_exact(c["offsets"], c["host"], c["rewards"], c["p"], gmax=gmax, rule=rule,
+                              wmax=wmax)
+    assert int(got["status"].item()) == 0
+    mse, bias = got["mse"].cpu().numpy(), got["bias_norm"].cpu().numpy()
+    zero = want["mse"] == 0.0                    # equal rewards: every edge vector is 0
+    assert np.all(mse[zero] == 0.0) and np.all(bias[zero] == 0.0)
+    live = ~zero
+    m_err = np.max(np.abs(mse[live] - want["mse"][live]) / want["mse"][live]) if live.any() else 0.0
+    b_abs = np.abs(bias - want["bias_norm"])
+    b_ok = (b_abs <= 2e-3 * want["bias_norm"]) | (b_abs <= 1e-4 * np.sqrt(want["mse"]))
+    log(f"  max mse rel {m_err:.2e}, max bias abs {b_abs.max():.2e}")
+    assert m_err <= BF16_TOL and b_ok.all()
