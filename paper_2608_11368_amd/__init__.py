@@ -21,7 +21,9 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libpair.so")
+# PAIR_LIB names another build of the same library to load instead (the test
+# suite's host-sanitizer build); it must exist like the default one.
+LIB_PATH = os.environ.get("PAIR_LIB") or os.path.join(_HERE, "libpair.so")
 
 PAIR_F32 = 0
 PAIR_BF16 = 1
