@@ -168,9 +168,10 @@ int pair_design_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offset
  * n_b = round(sum_i pi_target_i) of the G_b candidates continue, each with
  * first-order probability pi_target_i (the target is scaled by n_b / sum to
  * sum to n_b exactly).  Samples S of size n_b have probability
- * prod_{i in S} w_i / e_n(w) with odds w fitted here in fp64 (multiplicative
- * fixed point w_i <- w_i (pi_target_i / pi_i(w))^alpha, over-relaxed until
- * the error first grows, to 1e-12 relative), and the
+ * prod_{i in S} w_i / e_n(w) with odds w fitted here in fp64 (Newton's
+ * method on the log-odds, the Hessian being the design's own covariance
+ * pi_ij - pi_i pi_j, with step halving; to 1e-12 relative on every pi_i), and
+ * the
  * exact joint probabilities
  *     pi_ij = w_i w_j e_{n-2}(w without i, j) / e_n(w)
  * do not factorise; they are what the estimator must weight with.
@@ -182,11 +183,12 @@ int pair_design_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offset
  *   pi_joint       fp32 [B][gmax][gmax] out: pi_ij for i != j < G_b, pi_i on the
  *                  diagonal, 0 beyond G_b -- the pi block that
  *                  pair_edge_coeffs and pair_audit_rule take       (or NULL)
- *   iters          int32 [B] out: fixed-point iterations (negative: not
- *                  converged in 4000)                               (or NULL)
- * Device status: PAIR_ST_BAD_GROUP; PAIR_ST_P_RANGE (a target outside (0, 1),
- * a sum not within 1e-4 of an admissible integer, or no convergence: that
- * prompt's w is 0 and n_b = 0).
+ *   iters          int32 [B] out: evaluations of pi(w), halved steps
+ *                  included (negative: not converged in 200)        (or NULL)
+ * Device status: PAIR_ST_BAD_GROUP; PAIR_ST_P_RANGE (a target outside (0, 1)
+ * or a sum not within 1e-4 of an admissible integer: that prompt's w is 0,
+ * n_b = 0 and iters 0; no convergence: the last odds are written and iters
+ * is negative).
  */
 int pair_cps_fit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                  const float* pi_target, double* w, int32_t* n_out, float* pi_joint,

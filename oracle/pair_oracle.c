@@ -687,6 +687,12 @@ int orc_cps_fit(const double* pi_target, int64_t g, int64_t n, double tol, int64
         }
         w[i] = tg[i] / (1.0 - tg[i]);
     }
+    {   /* start at a geometric mean of 1 too, so the output always has it */
+        double lg0 = 0.0;
+        for (int64_t i = 0; i < g; ++i) lg0 += log(w[i]);
+        lg0 = exp(-lg0 / (double)g);
+        for (int64_t i = 0; i < g; ++i) w[i] *= lg0;
+    }
     int64_t it = 0;
     int ok = 0;
     for (; it < max_iter; ++it) {

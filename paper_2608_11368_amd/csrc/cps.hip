@@ -17,12 +17,13 @@
 //                   and one multiply-add), and lane i gets the leave-one-out
 //                   coefficient e_{n-1}(w without i) as the convolution
 //                   sum_k prefix_i[k] suffix_i[n-1-k] (all terms positive);
-//                   the odds follow the multiplicative fixed point
-//                   w_i <- w_i (pi_target_i / pi_i(w))^alpha, over-relaxed
-//                   with alpha = 1.8 until the error first grows and with
-//                   alpha = 1 from then on, renormalised to a geometric mean
-//                   of 1, until every pi_i is within 1e-12 of its target
-//                   (the fixed point is the same for every alpha).  The joint block uses the difference formula
+//                   the log-odds then take a Newton step whose Hessian is
+//                   the design covariance pi_ij - pi_i pi_j (solved by
+//                   Gaussian elimination in LDS, lane = row), halved until
+//                   the concave objective rises, until every pi_i is within
+//                   1e-12 of its target (3-8 evaluations where a plain
+//                   fixed point w_i <- w_i pi_target_i / pi_i takes
+//                   100-500).  The joint block uses the difference formula
 //                   when the two odds differ by more than 1% and the direct
 //                   leave-two-out polynomial otherwise.
 //  cps_draw_kernel  lane = replicate.  The workgroup builds the suffix table
@@ -42,7 +43,7 @@ namespace pair {
 
 namespace {
 
-constexpr int kMaxFitIter = 4000;
+constexpr int kMaxFitIter = 200;   // evaluations of pi(w), rejected steps included
 
 // e_0..e_{KP-1} (only k <= n meaningful) of the units 0..g-1 excluding skip1
 // and skip2, the units' odds taken from the wave (lane m holds w_m).
@@ -133,31 +134,113 @@ __global__ __launch_bounds__(kWave) void cps_fit_kernel(
     return;
   }
 
-  double w = unit ? t / (1.0 - t) : 0.0;
-  double e[KP];
+  // Newton's method on the log-odds theta (mean zero, so the geometric mean
+  // of the odds is 1).  The fitted odds maximise the concave
+  //     F(theta) = sum_i t_i theta_i - log e_n(exp(theta)),
+  // whose gradient is t - pi(theta) and whose negative Hessian is the
+  // design's covariance H_ij = pi_ij - pi_i pi_j (H_ii = pi_i (1 - pi_i)).
+  // H 1 = 0 (the odds are defined up to scale), so the step solves
+  // (H + 1 1^T / g) d = t - pi, whose solution is orthogonal to 1.  A step
+  // is kept when F rises by at least 1e-4 of the predicted amount or the
+  // largest relative error falls; otherwise it is halved.
+  // Wave reductions and lane reads run in uniform control flow: every lane
+  // takes part, and lanes beyond the group contribute 0.
+  double th = unit ? log(t / (1.0 - t)) : 0.0;
+  const double mean0 = wave_sum_d(th) / (double)g;
+  th = unit ? th - mean0 : 0.0;
+  double w = 0.0, pi = 0.0;
+  double th0 = 0.0, d = 0.0, f0 = 0.0, err0 = 0.0, slope = 0.0, step = 1.0;
+  bool have_base = false;
   int it = 0;
   bool converged = false;
-  double alpha = 1.8, prev_err = 1e300;   // over-relaxed step, back to 1 if the error grows
+  double* A = Pf;   // the Newton system reuses the prefix table's storage
   for (; it < kMaxFitIter; ++it) {
+    w = unit ? exp(th) : 0.0;
     // pi_i(w) for every unit from the prefix and suffix polynomial tables.
     esp_tables<KP>(w, g, n, lane, Pf, Sf);
-    double pi = 0.0;
+    const double en = Pf[g * kS + n];
+    pi = 0.0;
     if (unit) {
       double e1 = 0.0;   // e_{n-1}(w without i) = sum_k Pf[i][k] Sf[i][n-1-k]
       for (int k = 0; k < n; ++k)
         e1 = __dadd_rn(e1, __dmul_rn(Pf[lane * kS + k], Sf[lane * kS + (n - 1 - k)]));
-      pi = w * e1 / Pf[g * kS + n];
+      pi = w * e1 / en;
     }
+    const double f = wave_sum_d(unit ? t * th : 0.0) - log(en);
     const double err = wave_max_d(unit ? fabs(pi / t - 1.0) : 0.0);
+    __syncthreads();   // every lane has read the tables before A overwrites them
+    if (have_base) {
+      const bool ok = isfinite(f) && isfinite(err) &&
+                      (f >= f0 + 1e-4 * step * slope || err < err0);
+      if (!ok && step > 1e-9) {
+        step *= 0.5;
+        th = unit ? th0 + step * d : 0.0;
+        continue;
+      }
+    }
     if (err <= 1e-12) {
       converged = true;
       break;
     }
-    if (err > prev_err) alpha = 1.0;
-    prev_err = err;
-    if (unit) w *= alpha == 1.0 ? t / pi : pow(t / pi, alpha);
-    const double lg = wave_sum_d(unit ? log(w) : 0.0) / (double)g;
-    w = unit ? w * exp(-lg) : 0.0;
+    th0 = th;
+    f0 = f;
+    err0 = err;
+    have_base = true;
+
+    // Row `lane` of H + 1 1^T / g.  Off the diagonal pi_ij comes from the
+    // difference formula; where two odds agree to 1e-6 it is numerically
+    // unreliable, and those entries share what the row identity
+    // sum_{j != i} pi_ij = (n - 1) pi_i leaves (exact for equal odds).
+    const double inv_g = 1.0 / (double)g;
+    double known = 0.0;
+    int nclose = 0;
+    for (int j = 0; j < g; ++j) {
+      const double wj = readlane_d(w, j), pj = readlane_d(pi, j);
+      if (unit && j != lane) {
+        if (fabs(wj - w) > 1e-6 * fmax(wj, w)) {
+          const double pij = (wj * pi - w * pj) / (wj - w);
+          known += pij;
+          A[lane * kS + j] = pij - pi * pj + inv_g;
+        } else {
+          ++nclose;
+        }
+      }
+    }
+    if (unit) A[lane * kS + lane] = pi * (1.0 - pi) + inv_g;
+    const bool fill = unit && nclose > 0;
+    const double share = fill ? ((double)(n - 1) * pi - known) / (double)nclose : 0.0;
+    if (__ballot(fill) != 0ull) {
+      for (int j = 0; j < g; ++j) {
+        const double wj = readlane_d(w, j), pj = readlane_d(pi, j);
+        if (fill && j != lane && !(fabs(wj - w) > 1e-6 * fmax(wj, w)))
+          A[lane * kS + j] = share - pi * pj + inv_g;
+      }
+    }
+    // Gaussian elimination (the matrix is symmetric positive definite, so no
+    // pivoting), lane i owning row i and the right-hand side entry x_i.
+    double x = unit ? t - pi : 0.0;
+    for (int k = 0; k < g; ++k) {
+      __syncthreads();
+      const double akk = A[k * kS + k];
+      const double xk = readlane_d(x, k);
+      if (lane > k && lane < g) {
+        const double m = A[lane * kS + k] / akk;
+        for (int j = k + 1; j < g; ++j) A[lane * kS + j] -= m * A[k * kS + j];
+        x -= m * xk;
+      }
+    }
+    __syncthreads();
+    for (int k = g - 1; k >= 0; --k) {
+      if (lane == k) x /= A[k * kS + k];
+      const double xk = readlane_d(x, k);
+      if (lane < k) x -= A[lane * kS + k] * xk;
+    }
+    d = unit ? x : 0.0;
+    slope = wave_sum_d(unit ? (t - pi) * d : 0.0);
+    step = 1.0;
+    th = unit ? th0 + d : 0.0;
+    const double mean = wave_sum_d(th) / (double)g;
+    th = unit ? th - mean : 0.0;
     __syncthreads();   // the tables are rebuilt by the next iteration
   }
   if (!converged && lane == 0) raise_status(d_status, PAIR_ST_P_RANGE);
@@ -169,6 +252,7 @@ __global__ __launch_bounds__(kWave) void cps_fit_kernel(
 
   if (pi_joint != nullptr) {
     // pi_i of every unit (lane), then row i of the joint block by lane i.
+    double e[KP];
     esp_excl<KP>(w, g, n, lane, -1, e);
     double pi = 0.0, en = 1.0;
     if (unit) {

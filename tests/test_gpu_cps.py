@@ -60,6 +60,62 @@ def test_fit_vs_oracle(B, G):
     assert worst_w <= 1e-9 and worst_p <= 1e-6
 
 
+def _hard_targets():
+    """Targets that stress the fit: all equal (the start is already the
+    answer), a few tied values, a wide spread, and half the units near 0 with
+    half near 1; sample sizes 1, 2, G/2 and G - 1; G from 2 to 64."""
+    r = np.random.default_rng(17)
+    out = []
+    for g in (2, 3, 7, 16, 40, 64):
+        for n in sorted({1, 2, g // 2, g - 1}):
+            if not 1 <= n < g:
+                continue
+            cands = [np.full(g, n / g), r.choice([0.2, 0.5, 0.7], g), r.uniform(0.001, 0.999, g),
+                     np.where(np.arange(g) % 2 == 0, r.uniform(1e-3, 1e-2, g), r.uniform(0.9, 1.0, g))]
+            if g % 2 == 0 and n == g // 2:
+                cands.append(np.where(np.arange(g) % 2 == 0, r.uniform(0.01, 0.03, g),
+                                      r.uniform(0.97, 0.99, g)))
+            for t in cands:
+                t = t * (n / t.sum())
+                if 0 < t.min() and t.max() < 0.999:
+                    out.append(t.astype(np.float32))
+    return out
+
+
+def test_fit_hard_targets_vs_oracle():
+    groups = _hard_targets()
+    sizes = np.array([t.size for t in groups])
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    tgt = np.concatenate(groups)
+    nv = int(offsets[-1])
+    log(f"cps fit hard targets: B={len(groups)} nv={nv}")
+    got = pair.cps_fit(_t(offsets), _t(tgt), 64, nv=nv)
+    torch.cuda.synchronize()
+    assert int(got["status"].item()) == 0
+    w, n, its = got["w"].cpu().numpy(), got["n"].cpu().numpy(), got["iters"].cpu().numpy()
+    pj = got["pi_joint"].cpu().numpy()
+    assert np.all(its >= 0)
+    worst_w, worst_p = 0.0, 0.0
+    for b in range(len(groups)):
+        lo, hi = offsets[b], offsets[b + 1]
+        g = hi - lo
+        nb = int(round(float(tgt[lo:hi].astype(np.float64).sum())))
+        assert n[b] == nb
+        ow, it = oracle.cps_fit(tgt[lo:hi], nb, max_iter=100000)
+        assert it >= 0
+        worst_w = max(worst_w, float(np.max(np.abs(w[lo:hi] / ow - 1))))
+        _, opij = oracle.cps_inclusion(ow, nb)
+        off = ~np.eye(g, dtype=bool)
+        if nb >= 2:
+            worst_p = max(worst_p, float(np.max(np.abs(pj[b, :g, :g] - opij)[off] / opij[off])))
+        else:
+            assert np.all(np.abs(pj[b, :g, :g][off]) <= 1e-12)
+        assert np.max(np.abs(np.diag(pj[b, :g, :g]) - np.diag(opij)) / np.diag(opij)) <= 1e-6
+    log(f"  max w rel {worst_w:.2e}, max pi_ij rel {worst_p:.2e}, evaluations max {its.max()}")
+    assert worst_w <= 1e-9 and worst_p <= 1e-6
+    assert its.max() <= 40
+
+
 @pytest.mark.parametrize("R", [1, 300])
 def test_draw_bit_exact(R):
     w_ = wl.WORKLOADS["ragged"].replace(B=40)

@@ -66,6 +66,15 @@ def test_fit_reproduces_target(g, n):
     assert abs(np.sum(np.log(w))) <= 1e-9 * g
 
 
+@pytest.mark.parametrize("g,n", [(2, 1), (7, 3), (16, 15)])
+def test_fit_of_equal_targets_is_equal_odds_with_unit_geometric_mean(g, n):
+    # Equal targets n/g are met by equal odds at once (simple random
+    # sampling); the returned odds still carry the scale convention.
+    w, it = oracle.cps_fit(np.full(g, n / g), n)
+    assert it == 0
+    np.testing.assert_allclose(w, 1.0, rtol=0, atol=1e-15)
+
+
 def test_draw_has_the_design_distribution():
     g, n, R = 6, 3, 60000
     rng = np.random.default_rng(1)
