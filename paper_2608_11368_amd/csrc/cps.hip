@@ -24,8 +24,8 @@
 //                   1e-12 of its target (3-8 evaluations where a plain
 //                   fixed point w_i <- w_i pi_target_i / pi_i takes
 //                   100-500).  The joint block uses the difference formula
-//                   when the two odds differ by more than 1% and the direct
-//                   leave-two-out polynomial otherwise.
+//                   when the two odds differ by more than 1e-5 relative and
+//                   the direct leave-two-out polynomial otherwise.
 //  cps_draw_kernel  lane = replicate.  The workgroup builds the suffix table
 //                   E[i][k] = e_k(w_i .. w_{G-1}) in LDS (lane k, units from
 //                   the last); each lane then walks the units in order and
@@ -148,7 +148,7 @@ __global__ __launch_bounds__(kWave) void cps_fit_kernel(
   double th = unit ? log(t / (1.0 - t)) : 0.0;
   const double mean0 = wave_sum_d(th) / (double)g;
   th = unit ? th - mean0 : 0.0;
-  double w = 0.0, pi = 0.0;
+  double w = 0.0, pi = 0.0, en_last = 1.0;
   double th0 = 0.0, d = 0.0, f0 = 0.0, err0 = 0.0, slope = 0.0, step = 1.0;
   bool have_base = false;
   int it = 0;
@@ -159,6 +159,7 @@ __global__ __launch_bounds__(kWave) void cps_fit_kernel(
     // pi_i(w) for every unit from the prefix and suffix polynomial tables.
     esp_tables<KP>(w, g, n, lane, Pf, Sf);
     const double en = Pf[g * kS + n];
+    en_last = en;
     pi = 0.0;
     if (unit) {
       double e1 = 0.0;   // e_{n-1}(w without i) = sum_k Pf[i][k] Sf[i][n-1-k]
@@ -187,54 +188,68 @@ __global__ __launch_bounds__(kWave) void cps_fit_kernel(
     err0 = err;
     have_base = true;
 
-    // Row `lane` of H + 1 1^T / g.  Off the diagonal pi_ij comes from the
-    // difference formula; where two odds agree to 1e-6 it is numerically
-    // unreliable, and those entries share what the row identity
+    // Row `lane` of H + 1 1^T / g, in registers (entry j in a[j], zero
+    // beyond the group).  Off the diagonal pi_ij comes from the difference
+    // formula; where two odds agree to 1e-6 it is numerically unreliable, and
+    // those entries share what the row identity
     // sum_{j != i} pi_ij = (n - 1) pi_i leaves (exact for equal odds).
     const double inv_g = 1.0 / (double)g;
+    double a[KP];
     double known = 0.0;
     int nclose = 0;
-    for (int j = 0; j < g; ++j) {
+#pragma unroll
+    for (int j = 0; j < KP; ++j) {
       const double wj = readlane_d(w, j), pj = readlane_d(pi, j);
-      if (unit && j != lane) {
-        if (fabs(wj - w) > 1e-6 * fmax(wj, w)) {
-          const double pij = (wj * pi - w * pj) / (wj - w);
-          known += pij;
-          A[lane * kS + j] = pij - pi * pj + inv_g;
-        } else {
-          ++nclose;
-        }
-      }
+      const bool off = unit && j < g && j != lane;
+      const bool sep = fabs(wj - w) > 1e-6 * fmax(wj, w);
+      const double pij = (off && sep) ? (wj * pi - w * pj) / (wj - w) : 0.0;
+      known += pij;
+      nclose += (off && !sep) ? 1 : 0;
+      a[j] = (off && sep) ? pij - pi * pj + inv_g
+                          : ((unit && j == lane) ? pi * (1.0 - pi) + inv_g : 0.0);
     }
-    if (unit) A[lane * kS + lane] = pi * (1.0 - pi) + inv_g;
-    const bool fill = unit && nclose > 0;
-    const double share = fill ? ((double)(n - 1) * pi - known) / (double)nclose : 0.0;
-    if (__ballot(fill) != 0ull) {
-      for (int j = 0; j < g; ++j) {
+    if (__ballot(nclose > 0) != 0ull) {
+      const double share = nclose > 0 ? ((double)(n - 1) * pi - known) / (double)nclose : 0.0;
+#pragma unroll
+      for (int j = 0; j < KP; ++j) {
         const double wj = readlane_d(w, j), pj = readlane_d(pi, j);
-        if (fill && j != lane && !(fabs(wj - w) > 1e-6 * fmax(wj, w)))
-          A[lane * kS + j] = share - pi * pj + inv_g;
+        const bool close = unit && j < g && j != lane && !(fabs(wj - w) > 1e-6 * fmax(wj, w));
+        if (close) a[j] = share - pi * pj + inv_g;
       }
     }
-    // Gaussian elimination (the matrix is symmetric positive definite, so no
-    // pivoting), lane i owning row i and the right-hand side entry x_i.
+    // Gaussian elimination without pivoting (the matrix is symmetric
+    // positive definite).  Lane i owns row i and right-hand side entry x_i.
+    // At step k every row is shifted left by k, so the pivot column is
+    // always a[0] and all register indices are compile-time constants; the
+    // pivot row (row k, shifted) and its right-hand side are kept in LDS
+    // (U, xs) for the back substitution.  Rows at or above the pivot compute
+    // values that are never used.
     double x = unit ? t - pi : 0.0;
+    double* U = Pf;          // U[k][j] = row k's entry k + j after step k
+    double* xs = Sf;         // right-hand side of pivot row k
     for (int k = 0; k < g; ++k) {
-      __syncthreads();
-      const double akk = A[k * kS + k];
-      const double xk = readlane_d(x, k);
-      if (lane > k && lane < g) {
-        const double m = A[lane * kS + k] / akk;
-        for (int j = k + 1; j < g; ++j) A[lane * kS + j] -= m * A[k * kS + j];
-        x -= m * xk;
+      if (lane == k) {
+#pragma unroll
+        for (int j = 0; j < KP; ++j) U[k * KP + j] = a[j];
+        xs[k] = x;
       }
-    }
-    __syncthreads();
-    for (int k = g - 1; k >= 0; --k) {
-      if (lane == k) x /= A[k * kS + k];
+      __syncthreads();
       const double xk = readlane_d(x, k);
-      if (lane < k) x -= A[lane * kS + k] * xk;
+      const double m = a[0] / U[k * KP];
+#pragma unroll
+      for (int j = 1; j < KP; ++j) a[j - 1] = a[j] - m * U[k * KP + j];
+      a[KP - 1] = 0.0;
+      x -= m * xk;
     }
+    // Back substitution, one column of U per step: lane i keeps the still
+    // unresolved part y_i of its equation and ends holding x_i.
+    double y = unit ? xs[lane] : 0.0;
+    for (int k = g - 1; k >= 0; --k) {
+      const double xk = readlane_d(y, k) / U[k * KP];
+      if (lane == k) y = xk;
+      if (lane < k) y -= U[lane * KP + (k - lane)] * xk;
+    }
+    x = y;
     d = unit ? x : 0.0;
     slope = wave_sum_d(unit ? (t - pi) * d : 0.0);
     step = 1.0;
@@ -251,29 +266,24 @@ __global__ __launch_bounds__(kWave) void cps_fit_kernel(
   }
 
   if (pi_joint != nullptr) {
-    // pi_i of every unit (lane), then row i of the joint block by lane i.
-    double e[KP];
-    esp_excl<KP>(w, g, n, lane, -1, e);
-    double pi = 0.0, en = 1.0;
-    if (unit) {
-      const double e1 = pick<KP>(e, n - 1);
-      en = pick<KP>(e, n) + w * e1;
-      pi = w * e1 / en;
-    }
+    // Row i of the joint block by lane i, from the last evaluation's pi and
+    // e_n(w).  The difference formula loses about eps / gap of relative
+    // accuracy, so it is used where the two odds differ by more than 1e-5
+    // (error below 1e-8, under the fp32 output's rounding); closer pairs
+    // take the leave-two-out polynomial.
     float* row = pi_joint + (b * (int64_t)gmax + lane) * gmax;
     for (int j = 0; j < gmax; ++j) {
       const double wj = readlane_d(w, j < g ? j : 0), pj = readlane_d(pi, j < g ? j : 0);
+      const bool pair_ij = unit && j < g && j != lane;
+      const bool sep = fabs(wj - w) > 1e-5 * fmax(wj, w);
       double v = 0.0;
-      if (unit && j < g) {
-        if (j == lane) {
-          v = pi;
-        } else if (fabs(wj - w) > 0.01 * fmax(wj, w)) {
-          v = (wj * pi - w * pj) / (wj - w);
-        } else if (n >= 2) {
-          double e2[KP];
-          esp_excl<KP>(w, g, n - 2, lane, j, e2);   // w of lane j is excluded too
-          v = w * wj * pick<KP>(e2, n - 2) / en;
-        }
+      if (unit && j == lane) v = pi;
+      if (pair_ij && sep) v = (wj * pi - w * pj) / (wj - w);
+      const bool direct = pair_ij && !sep && n >= 2;
+      if (__ballot(direct) != 0ull) {
+        double e2[KP];
+        esp_excl<KP>(w, g, n - 2, lane, j, e2);   // w of lane j is excluded too
+        if (direct) v = w * wj * pick<KP>(e2, n - 2) / en_last;
       }
       if (lane < gmax) row[j] = (float)v;
     }
