@@ -26,6 +26,7 @@ Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--no-cpu-baseline]
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -315,12 +316,64 @@ def _cpu_model():
 RULE_NAMES = ("ht", "unweighted", "ratio_ke", "clipped", "selfnorm", "marginal")
 
 
+class TimingEvent:
+    """A HIP event used only to measure time on a stream.  It is created with
+    hipEventDisableSystemFence: recording it then does not write back and
+    invalidate the caches, which with default events adds several
+    microseconds to the work around each event and perturbs the kernel that
+    follows.  Elapsed times are read only after a device synchronisation."""
+
+    _hip = None
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    @classmethod
+    def _lib(cls):
+        if cls._hip is None:
+            # The HIP runtime torch has already loaded (the one libpair uses too).
+            hip = ctypes.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD | os.RTLD_GLOBAL)
+            hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+            hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                ctypes.c_void_p]
+            hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            cls._hip = hip
+        return cls._hip
+
+    def __init__(self):
+        self.h = ctypes.c_void_p()
+        rc = self._lib().hipEventCreateWithFlags(ctypes.byref(self.h), self.DISABLE_SYSTEM_FENCE)
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
+
+    def record(self, stream):
+        rc = self._lib().hipEventRecord(self.h, ctypes.c_void_p(stream.cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+    def synchronize(self):
+        rc = self._lib().hipEventSynchronize(self.h)
+        if rc != 0:
+            raise RuntimeError(f"hipEventSynchronize failed ({rc})")
+
+    def elapsed_time(self, end) -> float:
+        ms = ctypes.c_float()
+        rc = self._lib().hipEventElapsedTime(ctypes.byref(ms), self.h, end.h)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return float(ms.value)
+
+    def __del__(self):
+        if self._hip is not None and self.h:
+            self._hip.hipEventDestroy(self.h)
+
+
 def _event_ms(stream, fn, reps):
     import torch
 
     fn()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+    e0 = TimingEvent()
+    e1 = TimingEvent()
     e0.record(stream)
     for _ in range(reps):
         fn()
@@ -402,8 +455,8 @@ def time_alloc(pair, stream, wl, dev, reps=5):
                 pair.pair_design_alloc(B, nv, meta.gmax, off, ph, ch, None, bu, 0.08, design, pi,
                                        obj, its, st, stream)
             run()
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
+            e0 = TimingEvent()
+            e1 = TimingEvent()
             e0.record(stream)
             for _ in range(reps):
                 run()
@@ -444,8 +497,8 @@ def time_cps(pair, stream, wl, dev, reps=5, R=1):
                          ("draw_ms", lambda: pair.pair_cps_draw(B, nv, G, off, wv, n, 7, 0, R,
                                                                 mask, None, st, stream))):
             fn()
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
+            e0 = TimingEvent()
+            e1 = TimingEvent()
             e0.record(stream)
             for _ in range(reps):
                 fn()
@@ -475,8 +528,8 @@ def time_exact_audit(pair, stream, B, nv, G, off, scores, rew, p, D, reps=10):
             pair.pair_audit_exact(B, nv, G, off, scores, rew, p, None, 0, 0.0, mse, bias, None, ws,
                                   st, stream)
         run()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
+        e0 = TimingEvent()
+        e1 = TimingEvent()
         e0.record(stream)
         for _ in range(reps):
             run()
@@ -521,8 +574,8 @@ def time_variants(pair, stream, B, nv, G, off, rew, mask, pi, coeff, audit_args,
             res = {}
             for key, fn in (("coeffs_us", coeffs), ("audit_ms", audit)):
                 fn()
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
+                e0 = TimingEvent()
+                e1 = TimingEvent()
                 e0.record(stream)
                 for _ in range(reps):
                     fn()
@@ -553,14 +606,15 @@ def copy_calibration(gib=1.0, reps=5):
         dst.copy_(src)
         big.sum()
     torch.cuda.synchronize()
-    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-    e[0].record()
+    e = [TimingEvent() for _ in range(3)]
+    cur = torch.cuda.current_stream()
+    e[0].record(cur)
     for _ in range(reps):
         dst.copy_(src)
-    e[1].record()
+    e[1].record(cur)
     for _ in range(reps):
         big.sum()
-    e[2].record()
+    e[2].record(cur)
     torch.cuda.synchronize()
     copy_ms = e[0].elapsed_time(e[1]) / reps
     read_ms = e[1].elapsed_time(e[2]) / reps
@@ -651,7 +705,7 @@ def main():
         ev[3].record(stream)
 
     def events():
-        return [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        return [TimingEvent() for _ in range(4)]
 
     with torch.cuda.stream(stream):
         for _ in range(args.warmup):
