@@ -122,7 +122,7 @@ def _load():
         lib.orc_pair_coeffs_rule.argtypes = [i64, P, i32, P, P, P, ctypes.c_int, dbl, P, P, P, P]
         lib.orc_pair_coeffs_rule.restype = ctypes.c_int
         lib.orc_audit_rule.argtypes = [i64, P, i32, i64, P, ctypes.c_int, i64, P, P, P,
-                                       ctypes.c_int, dbl, u64, i64, i64, P, P, P, P, P]
+                                       ctypes.c_int, dbl, u64, i64, i64, P, P, P, P, P, P, P]
         lib.orc_audit_rule.restype = ctypes.c_int
         lib.orc_audit_exact.argtypes = [i64, P, i32, i64, P, ctypes.c_int, i64, P, P, P,
                                         ctypes.c_int, dbl, P, P]
@@ -294,7 +294,9 @@ def pair_coeffs(offsets, rewards, mask=None, pi=None, gmax=None):
 def audit(offsets, scores, rewards, p, seed, rep0, R, pi_w=None, gmax=None, prompt_id=None,
           want_reps=True, rule=RULE_HT, wmax=0.0):
     """Frozen-population audit of the estimator under `rule`: returns
-    dict(mse[B], bias_norm[B], rep_sqerr[B][R], edge_count[B][R])."""
+    dict(mse[B], bias_norm[B], rep_sqerr[B][R], edge_count[B][R], cosine[B],
+    target_norm[B]); cosine is the mean over replicates of the cosine between
+    each estimate and the target (0 for a zero estimate or target)."""
     lib = _load()
     off = _offsets(offsets)
     B = off.size - 1
@@ -310,12 +312,15 @@ def audit(offsets, scores, rewards, p, seed, rep0, R, pi_w=None, gmax=None, prom
     pid = None if prompt_id is None else np.ascontiguousarray(prompt_id, dtype=np.int64)
     mse = np.zeros(B, dtype=np.float64)
     bias = np.zeros(B, dtype=np.float64)
+    cos = np.zeros(B, dtype=np.float64)
+    tn = np.zeros(B, dtype=np.float64)
     reps = np.zeros((B, R), dtype=np.float64) if want_reps else None
     ec = np.zeros((B, R), dtype=np.int32) if want_reps else None
     _check(lib.orc_audit_rule(B, _ptr(off), gmax, D, _ptr(s), code, ld, _ptr(r), _ptr(pp),
                               _ptr(pi_w), int(rule), float(wmax), seed, rep0, R, _ptr(pid),
-                              _ptr(mse), _ptr(bias), _ptr(reps), _ptr(ec)))
-    return {"mse": mse, "bias_norm": bias, "rep_sqerr": reps, "edge_count": ec}
+                              _ptr(mse), _ptr(bias), _ptr(reps), _ptr(ec), _ptr(cos), _ptr(tn)))
+    return {"mse": mse, "bias_norm": bias, "rep_sqerr": reps, "edge_count": ec, "cosine": cos,
+            "target_norm": tn}
 
 
 def audit_exact(offsets, scores, rewards, p, pi_w=None, gmax=None, rule=RULE_HT, wmax=0.0):

@@ -411,12 +411,18 @@ int orc_pair_coeffs(int64_t B, const int64_t* offsets, int32_t gmax, const float
 /*       e_r = || g_r - t ||^2                                               */
 /*   mse  = (1/R) sum_r e_r ;  bias = || (1/R) sum_r g_r - t ||              */
 /* rep_sqerr[b][R] and edge_count[b][R] are optional per-replicate outputs. */
+/* Update direction (Sec. 5.2 and the audit matrix of App. E: the cosine    */
+/* between an estimate and the target): cos_r = <g_r, t> / (|g_r| |t|),     */
+/* taken as 0 when either vector is zero (a draw with no observed edge, or  */
+/* a prompt whose target vanishes); cosine[b] = (1/R) sum_r cos_r and       */
+/* target_norm[b] = |t| are optional outputs.                               */
 /* ------------------------------------------------------------------------ */
 int orc_audit_rule(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D,
                    const void* scores, int dtype, int64_t ld, const float* rewards,
                    const float* p, const float* pi_w, int rule, double wmax, uint64_t seed,
                    int64_t rep0, int64_t R, const int64_t* prompt_id, double* mse,
-                   double* bias_norm, double* rep_sqerr, int32_t* edge_count) {
+                   double* bias_norm, double* rep_sqerr, int32_t* edge_count, double* cosine,
+                   double* target_norm) {
     int st = check_offsets(B, offsets, gmax);
     if (st) return st;
     st = check_rule(rule, wmax);
@@ -450,7 +456,9 @@ int orc_audit_rule(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D,
         }
         if (s == ORC_OK)
             s = ht_estimate_one(o, g, D, scores, dtype, ld, rewards, NULL, NULL, gmax, t, NULL);
-        double esum = 0.0;
+        double tt = 0.0;
+        for (int64_t d = 0; s == ORC_OK && d < D; ++d) tt += t[d] * t[d];
+        double esum = 0.0, csum = 0.0;
         for (int64_t r = 0; s == ORC_OK && r < R; ++r) {
             for (int64_t i = 0; i < g; ++i)
                 m[o + i] = (uint8_t)orc_draw_indicator(seed, rep0 + r, bid, i, p[o + i]);
@@ -458,13 +466,16 @@ int orc_audit_rule(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D,
             s = rule_estimate_one(o, g, D, scores, dtype, ld, rewards, m, blk, gmax, rule, wmax, gr,
                                   &ke, NULL, NULL);
             if (s) break;
-            double e = 0.0;
+            double e = 0.0, gt = 0.0, gg = 0.0;
             for (int64_t d = 0; d < D; ++d) {
                 double dev = gr[d] - t[d];
                 e += dev * dev;
                 gsum[d] += gr[d];
+                gt += gr[d] * t[d];
+                gg += gr[d] * gr[d];
             }
             esum += e;
+            if (gg > 0.0 && tt > 0.0) csum += gt / (sqrt(gg) * sqrt(tt));
             if (rep_sqerr) rep_sqerr[b * R + r] = e;
             if (edge_count) edge_count[b * R + r] = ke;
         }
@@ -476,6 +487,8 @@ int orc_audit_rule(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D,
             }
             if (mse) mse[b] = esum / (double)R;
             if (bias_norm) bias_norm[b] = sqrt(bb);
+            if (cosine) cosine[b] = csum / (double)R;
+            if (target_norm) target_norm[b] = sqrt(tt);
         } else {
 #pragma omp critical
             err = s;
@@ -490,7 +503,8 @@ int orc_audit(int64_t B, const int64_t* offsets, int32_t gmax, int64_t D, const 
               uint64_t seed, int64_t rep0, int64_t R, const int64_t* prompt_id, double* mse,
               double* bias_norm, double* rep_sqerr, int32_t* edge_count) {
     return orc_audit_rule(B, offsets, gmax, D, scores, dtype, ld, rewards, p, pi_w, ORC_RULE_HT,
-                          0.0, seed, rep0, R, prompt_id, mse, bias_norm, rep_sqerr, edge_count);
+                          0.0, seed, rep0, R, prompt_id, mse, bias_norm, rep_sqerr, edge_count,
+                          NULL, NULL);
 }
 
 /* ------------------------------------------------------------------------ */

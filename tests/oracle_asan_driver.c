@@ -32,7 +32,8 @@ int orc_audit(int64_t, const int64_t*, int32_t, int64_t, const void*, int, int64
               const int64_t*, double*, double*, double*, int32_t*);
 int orc_audit_rule(int64_t, const int64_t*, int32_t, int64_t, const void*, int, int64_t,
                    const float*, const float*, const float*, int, double, uint64_t, int64_t,
-                   int64_t, const int64_t*, double*, double*, double*, int32_t*);
+                   int64_t, const int64_t*, double*, double*, double*, int32_t*, double*,
+                   double*);
 int orc_audit_exact(int64_t, const int64_t*, int32_t, int64_t, const void*, int, int64_t,
                     const float*, const float*, const float*, int, double, double*, double*);
 int orc_cps_inclusion(const double*, int64_t, int64_t, double*, double*);
@@ -149,8 +150,16 @@ static void run_case(int64_t c) {
                    (c & 2) ? pid : NULL, mse, bias, reps, rec) == 0, "audit", c);
   expect(all_finite(mse, B) && all_finite(bias, B) && all_finite(reps, B * R), "audit finite", c);
   for (int rule = 0; rule <= 5; ++rule) {
+    double* cosv = xmalloc((size_t)B * sizeof(double));
+    double* tnorm = xmalloc((size_t)B * sizeof(double));
     int rc = orc_audit_rule(B, off, gmax, D, scores, bf16, ld, rewards, p, pi_w, rule, 2.0, seed,
-                            rep0, R, NULL, mse, bias, NULL, NULL);
+                            rep0, R, NULL, mse, bias, NULL, NULL, cosv, tnorm);
+    if (rc == 0) {
+      expect(all_finite(cosv, B) && all_finite(tnorm, B), "audit cosine finite", c);
+      for (int64_t b = 0; b < B; ++b) expect(fabs(cosv[b]) <= 1.0 + 1e-12, "cosine in [-1, 1]", c);
+    }
+    free(cosv);
+    free(tnorm);
     expect(rc == 0, "audit_rule", c);
     rc = orc_audit_exact(B, off, gmax, D, scores, bf16, ld, rewards, p, pi_w, rule, 2.0, mse, bias);
     expect(rc == 0 || rc == -1, "audit_exact", c);

@@ -16,7 +16,7 @@ normaliser, the rho entry and the edge mask of the estimator (Eq. pair-ht);
 the half-edge split of the sequence advantages (Eq. pair-advantage); the
 Philox reading of the design draw (word, counter layout, key schedule), the
 induced-edge count and the logged rho block; bf16 widening; the audit's
-target, MSE and bias (App. D); the exact covariance trace of Prop. 1; the
+target, MSE, bias and update-direction cosine (App. D, Sec. 5.2); the exact covariance trace of Prop. 1; the
 conditional-Poisson inclusion probabilities; and the contrast graph's
 disagreement, edge proxy and vertex term, the design objective, its gradient
 and budget, and the pointwise and uniform comparison designs (Sec. 3.3-3.4).
@@ -75,6 +75,12 @@ MUTATIONS = [
     ("induced-edge count includes self pairs",
      "/* brute-force count of induced edges */\n                for (int64_t j = i + 1; j < g; ++j)",
      "/* brute-force count of induced edges */\n                for (int64_t j = i; j < g; ++j)"),
+    ("audit cosine against the estimate's own norm",
+     "if (gg > 0.0 && tt > 0.0) csum += gt / (sqrt(gg) * sqrt(tt));",
+     "if (gg > 0.0 && tt > 0.0) csum += gt / (sqrt(gg) * sqrt(gg));"),
+    ("audit cosine: a zero estimate counted as aligned",
+     "if (gg > 0.0 && tt > 0.0) csum += gt / (sqrt(gg) * sqrt(tt));",
+     "csum += (gg > 0.0 && tt > 0.0) ? gt / (sqrt(gg) * sqrt(tt)) : 1.0;"),
     ("logged rho uses p_i twice",
      "val = (float)((double)p[o + i] * (double)p[o + j]);",
      "val = (float)((double)p[o + i] * (double)p[o + i]);"),

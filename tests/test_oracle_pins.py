@@ -377,6 +377,67 @@ def test_audit_replicates_obey_gram_identity():
     assert np.allclose(res["mse"], res["rep_sqerr"].mean(axis=1), rtol=1e-14, atol=0)
 
 
+def test_audit_cosine_obeys_gram_identity():
+    """Per-replicate cosine between estimate and target from the coefficients
+    alone: cos_r = A~ K a / (sqrt(A~ K A~) sqrt(a K a)), K = S S^T, a the
+    complete-pair coefficients (independent algebra); the mean over
+    replicates is the oracle's cosine, |t| = sqrt(a K a)."""
+    w = wl.WORKLOADS["audit"].replace(B=6, D=96, R=40)
+    meta = wl.host_meta(w)
+    s = wl.host_scores(w, meta.nv)
+    res = oracle.audit(meta.offsets, s, meta.rewards, meta.p, seed=w.design_seed, rep0=3, R=w.R)
+    d = oracle.design_inclusion(meta.offsets, meta.p, seed=w.design_seed, rep0=3, R=w.R,
+                                gmax=meta.gmax)
+    import torch
+
+    sf = torch.from_numpy(s.view(np.int16)).view(torch.bfloat16).double().numpy()
+    full, _ = oracle.pair_coeffs(meta.offsets, meta.rewards)
+    for b in range(meta.B):
+        o0, o1 = meta.offsets[b], meta.offsets[b + 1]
+        K = sf[o0:o1] @ sf[o0:o1].T
+        a = full[o0:o1]
+        tt = a @ K @ a
+        assert abs(res["target_norm"][b] - math.sqrt(tt)) <= 1e-12 * math.sqrt(tt)
+        cos = []
+        for r in range(w.R):
+            u, _ = oracle.pair_coeffs(np.array([0, o1 - o0], np.int64), meta.rewards[o0:o1],
+                                      d["mask"][r][o0:o1], d["pi"][b:b + 1])
+            uu = u @ K @ u
+            cos.append(u @ K @ a / math.sqrt(uu * tt) if uu > 0 and tt > 0 else 0.0)
+        assert abs(res["cosine"][b] - np.mean(cos)) <= 1e-10
+        assert -1.0 <= res["cosine"][b] <= 1.0
+
+
+def test_audit_cosine_special_cases():
+    """p = 1: every estimate is the target (cosine 1).  G = 2: a draw gives
+    t / rho when both candidates continue and 0 otherwise, so the cosine is
+    the fraction of such draws.  Equal rewards: zero target, cosine 0.
+    Rescaling scores or rewards leaves the cosine unchanged."""
+    w = wl.WORKLOADS["audit"].replace(B=4, D=40, R=30)
+    meta = wl.host_meta(w)
+    s = wl.host_scores(w, meta.nv)
+    one = oracle.audit(meta.offsets, s, meta.rewards, np.ones_like(meta.p), seed=1, rep0=0, R=5)
+    pos = one["target_norm"] > 0
+    assert np.all(np.abs(one["cosine"][pos] - 1.0) <= 1e-12)
+    assert np.all(one["cosine"][~pos] == 0.0)
+
+    rng = np.random.default_rng(5)
+    off = np.array([0, 2, 4, 6], np.int64)
+    r2 = np.array([1, 0, 0.3, 0.9, 0.5, 0.5], np.float32)        # last prompt: equal rewards
+    p2 = np.array([0.6, 0.7, 0.4, 0.9, 0.5, 0.8], np.float32)
+    s2 = rng.standard_normal((6, 17)).astype(np.float32)
+    R = 400
+    res = oracle.audit(off, s2, r2, p2, seed=9, rep0=11, R=R)
+    d = oracle.design_inclusion(off, p2, seed=9, rep0=11, R=R, gmax=2)
+    for b in range(2):
+        both = np.mean(d["mask"][:, 2 * b] & d["mask"][:, 2 * b + 1])
+        assert abs(res["cosine"][b] - both) <= 1e-12
+    assert res["target_norm"][2] == 0.0 and res["cosine"][2] == 0.0
+    scaled = oracle.audit(off, (3.0 * s2).astype(np.float32), (2.0 * r2).astype(np.float32), p2,
+                          seed=9, rep0=11, R=R)
+    assert np.allclose(scaled["cosine"], res["cosine"], rtol=0, atol=1e-12)
+
+
 def test_audit_p_one_has_zero_error():
     w = wl.WORKLOADS["audit"].replace(B=3, D=40, R=5)
     meta = wl.host_meta(w)
