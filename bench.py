@@ -558,6 +558,10 @@ def time_variants(pair, stream, B, nv, G, off, rew, mask, pi, coeff, audit_args,
     dev = coeff.device
     ess = torch.empty(B, dtype=torch.float32, device=dev)
     mw = torch.empty(B, dtype=torch.float32, device=dev)
+    cos = torch.empty(Ba, dtype=torch.float64, device=dev)
+    tnorm = torch.empty(Ba, dtype=torch.float64, device=dev)
+    wsd = torch.empty(pair.pair_audit_direction_workspace_bytes(Ba, Ga, scores_a.shape[1], R),
+                      dtype=torch.uint8, device=dev)
     out = {}
     with torch.cuda.stream(stream):
         for rule, name in enumerate(RULE_NAMES):
@@ -571,8 +575,14 @@ def time_variants(pair, stream, B, nv, G, off, rew, mask, pi, coeff, audit_args,
                 pair.pair_audit_rule(Ba, nva, Ga, off_a, scores_a, rew_a, p_a, None, rule, wmax,
                                      wa.design_seed, 0, R, mse, bias, rps, ec_a, ws, status, stream)
 
+            def direction():
+                pair.pair_audit_direction(Ba, nva, Ga, off_a, scores_a, rew_a, p_a, None, rule,
+                                          wmax, wa.design_seed, 0, R, cos, tnorm, wsd, status,
+                                          stream)
+
             res = {}
-            for key, fn in (("coeffs_us", coeffs), ("audit_ms", audit)):
+            for key, fn in (("coeffs_us", coeffs), ("audit_ms", audit),
+                            ("direction_ms", direction)):
                 fn()
                 e0 = TimingEvent()
                 e1 = TimingEvent()
@@ -585,6 +595,8 @@ def time_variants(pair, stream, B, nv, G, off, rew, mask, pi, coeff, audit_args,
                 res[key] = round(t * 1e3 if key == "coeffs_us" else t, 4)
             res["audit_mean_mse"] = float(mse.mean().item())
             res["audit_mean_bias"] = float(bias.mean().item())
+            live = tnorm > 0
+            res["audit_mean_cosine"] = round(float(cos[live].mean().item()), 6)
             res["b128_mean_ess"] = round(float(ess.mean().item()), 3)
             out[name] = res
     if int(status.item()) != 0:

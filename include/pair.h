@@ -364,6 +364,42 @@ int pair_audit_rule(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                     void* stream);
 
 /*
+ * pair_audit_direction_workspace_bytes -- device workspace that
+ * pair_audit_direction needs for B prompts of at most gmax vertices, D score
+ * columns and R replicates (0 when a size is out of range).
+ */
+size_t pair_audit_direction_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R);
+
+/*
+ * pair_audit_direction -- the update-direction column of the frozen-policy
+ * audit (paper Sec. 5.2 lists the cosine among the audit metrics; the audit
+ * matrix of App. E reports it per design): for the replicates rep0 ..
+ * rep0+R-1, drawn and folded exactly as pair_audit_rule draws and folds them,
+ *     cos_r     = <g_r, t> / (|g_r| |t|)    (0 when g_r = 0 or t = 0)
+ *     cosine[b] = (1/R) sum_r cos_r,   target_norm[b] = |t|,
+ * with g_r the replicate's estimate under `rule` and t the complete-pair
+ * target.  It is evaluated through the prompt's Gram matrix K = S_b S_b^T
+ * (fp64 from fp32 matrix-core partial sums): with u_r the replicate's
+ * coefficients and a the target's, cos_r = u_r K a / sqrt(u_r K u_r a K a).
+ * A prompt whose target is zero (equal rewards) reports cosine 0 and
+ * target_norm 0.
+ *
+ *   arguments      as pair_audit_rule (PAIR_BF16 scores only)
+ *   cosine, target_norm  fp64 [B] out
+ *   workspace      device scratch of ws_bytes >=
+ *                  pair_audit_direction_workspace_bytes, 256-byte aligned;
+ *                  contents on entry do not matter
+ * Device status: PAIR_ST_BAD_GROUP, PAIR_ST_P_RANGE, PAIR_ST_RHO_RANGE,
+ * PAIR_ST_NONFINITE.
+ */
+int pair_audit_direction(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                         const void* scores, int32_t dtype, int64_t ld, const float* rewards,
+                         const float* p, const float* pi_w, int32_t rule, float wmax,
+                         uint64_t seed, int64_t rep0, int64_t R, double* cosine,
+                         double* target_norm, void* workspace, size_t ws_bytes,
+                         int32_t* d_status, void* stream);
+
+/*
  * pair_audit_exact_workspace_bytes -- device workspace that pair_audit_exact
  * needs for B prompts of at most gmax vertices and D score columns.
  */

@@ -46,7 +46,8 @@ RULE_MARGINAL = 5
 
 EXPORTED = ("pair_design_coeffs", "pair_design_alloc", "pair_cps_fit", "pair_cps_draw", "pair_design_inclusion", "pair_edge_coeffs", "pair_edge_coeffs_rule",
             "pair_weighted_grad", "pair_audit_workspace_bytes", "pair_audit", "pair_audit_rule",
-            "pair_audit_exact_workspace_bytes", "pair_audit_exact", "pair_strerror",
+            "pair_audit_exact_workspace_bytes", "pair_audit_exact",
+            "pair_audit_direction_workspace_bytes", "pair_audit_direction", "pair_strerror",
             "pair_version")
 
 
@@ -86,6 +87,11 @@ def lib() -> ctypes.CDLL:
         L.pair_audit_exact.restype = ctypes.c_int
         L.pair_design_alloc.argtypes = [i64, i64, i32, P, P, P, P, P, f32, i32, P, P, P, P, P]
         L.pair_design_alloc.restype = ctypes.c_int
+        L.pair_audit_direction_workspace_bytes.argtypes = [i64, i32, i64, i64]
+        L.pair_audit_direction_workspace_bytes.restype = ctypes.c_size_t
+        L.pair_audit_direction.argtypes = [i64, i64, i32, P, i64, P, i32, i64, P, P, P, i32, f32,
+                                           u64, i64, i64, P, P, P, ctypes.c_size_t, P, P]
+        L.pair_audit_direction.restype = ctypes.c_int
         L.pair_design_coeffs.argtypes = [i64, i64, i32, P, P, P, u64, i64, P, P, P, P, P, P, P]
         L.pair_design_coeffs.restype = ctypes.c_int
         L.pair_cps_fit.argtypes = [i64, i64, i32, P, P, P, P, P, P, P, P]
@@ -277,6 +283,24 @@ def pair_audit_rule(B, nv, gmax, offsets, scores, rewards, p, pi_w, rule, wmax, 
         _stream(stream)), _name)
 
 
+def pair_audit_direction_workspace_bytes(B, gmax, D, R) -> int:
+    return int(lib().pair_audit_direction_workspace_bytes(B, gmax, D, R))
+
+
+def pair_audit_direction(B, nv, gmax, offsets, scores, rewards, p, pi_w, rule, wmax, seed, rep0,
+                         R, cosine, target_norm, workspace, d_status=None, stream=None):
+    sp, code, ld, D = _scores_arg(scores)
+    ws = _dev(workspace, "workspace", torch.uint8)
+    _rc(lib().pair_audit_direction(
+        B, nv, gmax, _dev(offsets, "offsets", torch.int64, B + 1), D, sp, code, ld,
+        _dev(rewards, "rewards", torch.float32, nv), _dev(p, "p", torch.float32, nv),
+        _dev(pi_w, "pi_w", torch.float32, B * gmax * gmax, True), int(rule), float(wmax),
+        ctypes.c_uint64(seed & ((1 << 64) - 1)), rep0, R,
+        _dev(cosine, "cosine", torch.float64, B), _dev(target_norm, "target_norm", torch.float64, B),
+        ws, workspace.numel(), _dev(d_status, "d_status", torch.int32, 1, True),
+        _stream(stream)), "pair_audit_direction")
+
+
 def pair_audit_exact_workspace_bytes(B, gmax, D) -> int:
     return int(lib().pair_audit_exact_workspace_bytes(B, gmax, D))
 
@@ -368,6 +392,25 @@ def audit(offsets, scores, rewards, p, seed, rep0, R, gmax, pi_w=None, want_reps
         pair_audit_rule(B, nv, gmax, offsets, scores, rewards, p, pi_w, rule, wmax, seed, rep0, R,
                         out["mse"], out["bias_norm"], out["rep_sqerr"], out["edge_count"],
                         workspace, out["status"], stream)
+    return out
+
+
+def audit_direction(offsets, scores, rewards, p, seed, rep0, R, gmax, pi_w=None, rule=RULE_HT,
+                    wmax=0.0, nv=None, workspace=None, stream=None):
+    """Mean per-replicate cosine between estimate and target, and |t|."""
+    B = offsets.numel() - 1
+    nv = _nv(offsets) if nv is None else nv
+    dev = scores.device
+    need = pair_audit_direction_workspace_bytes(B, gmax, scores.shape[1], R)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    out = {
+        "cosine": torch.empty(B, dtype=torch.float64, device=dev),
+        "target_norm": torch.empty(B, dtype=torch.float64, device=dev),
+        "status": torch.zeros(1, dtype=torch.int32, device=dev),
+    }
+    pair_audit_direction(B, nv, gmax, offsets, scores, rewards, p, pi_w, rule, wmax, seed, rep0, R,
+                         out["cosine"], out["target_norm"], workspace, out["status"], stream)
     return out
 
 

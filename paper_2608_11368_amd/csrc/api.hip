@@ -157,6 +157,39 @@ int pair_audit_rule(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                             as_stream(stream));
 }
 
+size_t pair_audit_direction_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R) {
+  if (B < 1 || gmax < 2 || gmax > PAIR_GMAX_LIMIT || D < 1 || D > kMaxCount || R < 1 ||
+      R > kMaxCount || B > kMaxCount / (R + 1))
+    return 0;
+  return pair::direction_workspace_bytes(B, gmax, D, R);
+}
+
+int pair_audit_direction(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                         const void* scores, int32_t dtype, int64_t ld, const float* rewards,
+                         const float* p, const float* pi_w, int32_t rule, float wmax,
+                         uint64_t seed, int64_t rep0, int64_t R, double* cosine,
+                         double* target_norm, void* workspace, size_t ws_bytes,
+                         int32_t* d_status, void* stream) {
+  int st = check_groups(B, nv, gmax, offsets);
+  if (st) return st;
+  st = check_rule(rule, wmax);
+  if (st) return st;
+  if (dtype != PAIR_BF16) return PAIR_EDTYPE;
+  st = check_scores(scores, dtype, D, ld);
+  if (st) return st;
+  if (rewards == nullptr || p == nullptr || cosine == nullptr || target_norm == nullptr)
+    return PAIR_EINVAL;
+  if (R < 1 || rep0 < 0 || R > kMaxCount || rep0 > kMaxCount) return PAIR_ERANGE;
+  const size_t need = pair_audit_direction_workspace_bytes(B, gmax, D, R);
+  if (need == 0) return PAIR_ERANGE;
+  if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 ||
+      ws_bytes < need)
+    return PAIR_EWORKSPACE;
+  return pair::launch_audit_direction(B, nv, gmax, offsets, D, scores, ld, rewards, p, pi_w, rule,
+                                      wmax, seed, rep0, R, cosine, target_norm, workspace,
+                                      d_status, as_stream(stream));
+}
+
 int pair_design_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                       const float* p_hat, const float* c_hat, const float* m_hat,
                       const float* budget, float pi_min, int32_t design, float* pi,

@@ -96,6 +96,22 @@ AuditLayout audit_layout(int64_t B, int32_t gmax, int64_t D, int64_t R) {
   return L;
 }
 
+// Complete-pair coefficient a_i of vertex `lane` (0 beyond the group): the
+// fold with every vertex completed and rho = 1, centred over all G vertices
+// (Theorem 1: (r_i - mean r) / (G - 1) in exact arithmetic).  The whole wave
+// calls it; lane i holds r_i.
+__device__ __forceinline__ float complete_pair_coeff(float r_i, int lane, int g) {
+  const bool vert = lane < g;
+  float cf = 0.0f;
+  for (int j = 0; j < g; ++j) {
+    const float r_j = lane_value(r_i, j);
+    if (vert && j != lane) cf += r_i - r_j;
+  }
+  float a_full = vert ? cf / (float)(g * (g - 1)) : 0.0f;
+  const float tot = wave_sum(a_full);
+  return vert ? a_full - tot / (float)g : 0.0f;
+}
+
 // ---------------------------------------------------------------------------
 // 1. Replicate coefficients.  A workgroup owns one prompt and 256 replicates
 //    (one per lane).  The edge table W, the probabilities and the
@@ -133,16 +149,7 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
       rl[lane] = r_i;
     }
     if (vert && !p_in_range(p_i) && chunk == 0) raise_status(d_status, PAIR_ST_P_RANGE);
-    // Complete-pair coefficients: the same fold with every vertex completed
-    // and rho = 1, centred over all G vertices.
-    float cf = 0.0f;
-    for (int j = 0; j < g; ++j) {
-      const float r_j = lane_value(r_i, j);
-      if (vert && j != lane) cf += r_i - r_j;
-    }
-    float a_full = vert ? cf / (float)(g * (g - 1)) : 0.0f;
-    const float tot = wave_sum(a_full);
-    a_full = vert ? a_full - tot / (float)g : 0.0f;
+    const float a_full = complete_pair_coeff(r_i, lane, (int)g);
     if (lane < KP) af[lane] = a_full;
   }
   __syncthreads();
@@ -616,10 +623,189 @@ __global__ __launch_bounds__(256) void audit_final_kernel(
   bias_norm[b] = sqrt((double)ebar[b]);
 }
 
+// ---------------------------------------------------------------------------
+// Update direction (Sec. 5.2 audit metrics; the Cosine column of the audit
+// matrix, App. E).  Replicate r's estimate is g_r = u_r S_b with
+// u_r = delta_r + a (its fold's coefficients) and the target is t = a S_b, so
+// with the fp64 Gram matrix K = S_b S_b^T
+//     cos_r = u_r K a / sqrt(u_r K u_r * a K a),
+// taken as 0 when either quadratic form is not positive (a draw with no
+// observed edge has u_r = 0 exactly; a prompt with equal rewards has a = 0).
+// A workgroup owns one prompt and 256 replicates (one per thread) and writes
+// the fixed-order sum of its cosines; a second kernel adds the chunks in
+// order.  a is recomputed exactly as audit_coeffs_kernel computes it, so
+// delta_r + a restores the fold's coefficients to within one fp32 rounding.
+// ---------------------------------------------------------------------------
+constexpr int kCosThreads = 256;
+
+template <int KP>
+__global__ __launch_bounds__(kCosThreads) void audit_cosine_kernel(
+    int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets,
+    const float* __restrict__ rewards, int64_t R, int64_t nwg, int64_t rrows,
+    const float* __restrict__ delta, const double* __restrict__ gram, double* __restrict__ cpart,
+    double* __restrict__ target_norm) {
+  constexpr int kWaves = kCosThreads / kWave;
+  __shared__ double K[KP * KP];
+  __shared__ double ka[KP];
+  __shared__ float af[KP];
+  __shared__ double red[kWaves];
+  __shared__ double tt_s;
+  const int64_t b = blockIdx.x / nwg;
+  const int64_t chunk = blockIdx.x - b * nwg;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  int64_t o0, g64;
+  if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g64, nullptr, false)) return;
+  const int g = (int)g64;
+
+  if (wave == 0) {
+    const float r_i = lane < g ? rewards[o0 + lane] : 0.0f;
+    const float a_full = complete_pair_coeff(r_i, lane, g);
+    if (lane < KP) af[lane] = a_full;
+  }
+  for (int idx = tid; idx < KP * KP; idx += kCosThreads) {
+    const int i = idx / KP, j = idx - i * KP;
+    K[idx] = (i < g && j < g) ? gram[(b * gmax + i) * (int64_t)gmax + j] : 0.0;
+  }
+  __syncthreads();
+  if (tid < KP) {
+    double v = 0.0;
+    for (int j = 0; j < g; ++j) v += K[tid * KP + j] * (double)af[j];
+    ka[tid] = v;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double t2 = 0.0;
+    for (int i = 0; i < g; ++i) t2 += (double)af[i] * ka[i];
+    tt_s = t2;
+    if (chunk == 0) target_norm[b] = t2 > 0.0 ? sqrt(t2) : 0.0;
+  }
+  __syncthreads();
+  const double tt = tt_s;
+
+  const int64_t rloc = chunk * kCosThreads + tid;
+  double cosv = 0.0;
+  if (rloc < R && tt > 0.0) {
+    const float* drow = delta + (b * rrows + rloc) * KP;
+    double u[KP];
+#pragma unroll
+    for (int i0 = 0; i0 < KP; i0 += 4) {
+      const float4 v4 = *reinterpret_cast<const float4*>(drow + i0);
+      u[i0] = (double)(v4.x + af[i0]);
+      u[i0 + 1] = (double)(v4.y + af[i0 + 1]);
+      u[i0 + 2] = (double)(v4.z + af[i0 + 2]);
+      u[i0 + 3] = (double)(v4.w + af[i0 + 3]);
+    }
+    double uka = 0.0, uku = 0.0;
+    for (int i = 0; i < g; ++i) {
+      double ki = 0.0;
+#pragma unroll
+      for (int j = 0; j < KP; ++j) ki += K[i * KP + j] * u[j];
+      double ui = 0.0;
+#pragma unroll
+      for (int q = 0; q < KP; ++q) ui = q == i ? u[q] : ui;
+      uku += ui * ki;
+      uka += ui * ka[i];
+    }
+    if (uku > 0.0) cosv = uka / sqrt(uku * tt);
+  }
+  // Fixed-order sum: butterfly within each wave, then the waves in order.
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) cosv += __shfl_xor(cosv, m, kWave);
+  if (lane == 0) red[wave] = cosv;
+  __syncthreads();
+  if (tid == 0) {
+    double sum = 0.0;
+    for (int w = 0; w < kWaves; ++w) sum += red[w];
+    cpart[b * nwg + chunk] = sum;
+  }
+}
+
+__global__ __launch_bounds__(256) void audit_cosine_final_kernel(
+    int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets, int64_t R,
+    int64_t nwg, const double* __restrict__ cpart, double* __restrict__ cosine) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  int64_t o0, g;
+  if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, nullptr, false)) return;
+  double sum = 0.0;
+  for (int64_t c = 0; c < nwg; ++c) sum += cpart[b * nwg + c];
+  cosine[b] = sum / (double)R;
+}
+
 }  // namespace
 
 size_t audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R) {
   return audit_layout(B, gmax, D, R).total;
+}
+
+// Workspace of launch_audit_direction: the Gram slice partials, the fp64
+// Gram matrices, the replicate deviations and their partial sums (as in the
+// audit), and the per-chunk cosine sums.
+struct DirectionLayout {
+  size_t gram_part_off, gram_off, delta_off, dsum_off, cpart_off, total;
+};
+
+DirectionLayout direction_layout(int64_t B, int32_t gmax, int64_t D, int64_t R) {
+  const AuditLayout A = audit_layout(B, gmax, D, R);
+  DirectionLayout L;
+  size_t off = 0;
+  L.gram_part_off = off;
+  off += (size_t)round_up((int64_t)exact_workspace_bytes(B, gmax, D), 256);
+  L.gram_off = off;
+  off += (size_t)round_up(B * (int64_t)gmax * gmax * 8, 256);
+  L.delta_off = off;
+  off += (size_t)round_up(B * A.rrows * A.kp * 4, 256);
+  L.dsum_off = off;
+  off += (size_t)round_up(B * A.nwg * gmax * 4, 256);
+  L.cpart_off = off;
+  off += (size_t)round_up(B * A.nwg * 8, 256);
+  L.total = off;
+  return L;
+}
+
+size_t direction_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R) {
+  return direction_layout(B, gmax, D, R).total;
+}
+
+int launch_audit_direction(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                           const void* scores, int64_t ld, const float* rewards, const float* p,
+                           const float* pi_w, int32_t rule, float wmax, uint64_t seed,
+                           int64_t rep0, int64_t R, double* cosine, double* target_norm,
+                           void* workspace, int32_t* d_status, hipStream_t stream) {
+  const AuditLayout A = audit_layout(B, gmax, D, R);
+  const DirectionLayout L = direction_layout(B, gmax, D, R);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  double* gram = reinterpret_cast<double*>(ws + L.gram_off);
+  float* delta = reinterpret_cast<float*>(ws + L.delta_off);
+  float* dsum = reinterpret_cast<float*>(ws + L.dsum_off);
+  double* cpart = reinterpret_cast<double*>(ws + L.cpart_off);
+
+  int st = launch_gram(B, nv, gmax, offsets, D, scores, ld, gram, ws + L.gram_part_off, d_status,
+                       stream);
+  if (st != PAIR_OK) return st;
+  const int64_t grid = B * A.nwg;
+  if (grid > 0x7fffffffLL) return PAIR_ERANGE;
+#define PAIR_DIR(KP_)                                                                           \
+  hipLaunchKernelGGL(audit_coeffs_kernel<KP_>, dim3((unsigned)grid), dim3(kCoefThreads), 0,      \
+                     stream, B, nv, gmax, offsets, rewards, p, pi_w, rule, wmax, seed, rep0, R,  \
+                     A.nwg, A.rrows, delta, dsum, nullptr, d_status);                           \
+  if (hipGetLastError() != hipSuccess) return PAIR_EHIP;                                        \
+  hipLaunchKernelGGL(audit_cosine_kernel<KP_>, dim3((unsigned)grid), dim3(kCosThreads), 0,       \
+                     stream, B, nv, gmax, offsets, rewards, R, A.nwg, A.rrows, delta, gram,       \
+                     cpart, target_norm)
+  switch (A.ks) {
+    case 1: PAIR_DIR(16); break;
+    case 2: PAIR_DIR(32); break;
+    case 3: PAIR_DIR(48); break;
+    default: PAIR_DIR(64); break;
+  }
+#undef PAIR_DIR
+  if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
+  hipLaunchKernelGGL(audit_cosine_final_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0,
+                     stream, B, nv, gmax, offsets, R, A.nwg, cpart, cosine);
+  return hipGetLastError() == hipSuccess ? PAIR_OK : PAIR_EHIP;
 }
 
 int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,

@@ -329,10 +329,67 @@ __global__ __launch_bounds__(kFinalThreads) void exact_final_kernel(
   }
 }
 
+// K = S_b S_b^T of every prompt in fp64 (the slice partials added in slice
+// order, as exact_final_kernel adds them), for callers that only need the
+// Gram matrices.  gram[b][i][j] for i, j < G_b; entries beyond are not
+// written.
+template <int KP>
+__global__ __launch_bounds__(kFinalThreads) void gram_sum_kernel(
+    int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets, int64_t nsl,
+    const float* __restrict__ part, double* __restrict__ gram, int32_t* d_status) {
+  const int64_t b = blockIdx.x;
+  int64_t o0, g;
+  if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, d_status, threadIdx.x == 0)) return;
+  const int gi = (int)g;
+  bool nonfinite = false;
+  for (int idx = threadIdx.x; idx < KP * KP; idx += kFinalThreads) {
+    const int i = idx / KP, j = idx - i * KP;
+    if (i >= gi || j >= gi) continue;
+    const float* src = part + b * nsl * (int64_t)KP * KP + idx;
+    double k = 0.0;
+    for (int64_t s = 0; s < nsl; ++s) k += (double)src[s * (int64_t)KP * KP];
+    if (!isfinite(k)) nonfinite = true;
+    gram[(b * gmax + i) * (int64_t)gmax + j] = k;
+  }
+  if (nonfinite) raise_status(d_status, PAIR_ST_NONFINITE);
+}
+
 }  // namespace
 
 size_t exact_workspace_bytes(int64_t B, int32_t gmax, int64_t D) {
   return exact_layout(B, gmax, D).total;
+}
+
+int launch_gram(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                const void* scores, int64_t ld, double* gram, void* workspace, int32_t* d_status,
+                hipStream_t stream) {
+  const ExactLayout L = exact_layout(B, gmax, D);
+  float* part = static_cast<float*>(workspace);
+  const uint16_t* s = static_cast<const uint16_t*>(scores);
+  const int64_t grid = B * L.nsl;
+  if (grid > 0x7fffffffLL) return PAIR_ERANGE;
+#define PAIR_GRAM(KS_)                                                                         \
+  hipLaunchKernelGGL(gram_kernel<KS_>, dim3((unsigned)grid), dim3(kGramThreads), 0, stream, B, \
+                     nv, gmax, offsets, D, s, ld, L.nsl, L.slice, part)
+#define PAIR_GSUM(KP_)                                                                        \
+  hipLaunchKernelGGL(gram_sum_kernel<KP_>, dim3((unsigned)B), dim3(kFinalThreads), 0, stream, \
+                     B, nv, gmax, offsets, L.nsl, part, gram, d_status)
+  switch (L.ks) {
+    case 1: PAIR_GRAM(1); break;
+    case 2: PAIR_GRAM(2); break;
+    case 3: PAIR_GRAM(3); break;
+    default: PAIR_GRAM(4); break;
+  }
+  if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
+  switch (L.ks) {
+    case 1: PAIR_GSUM(16); break;
+    case 2: PAIR_GSUM(32); break;
+    case 3: PAIR_GSUM(48); break;
+    default: PAIR_GSUM(64); break;
+  }
+#undef PAIR_GRAM
+#undef PAIR_GSUM
+  return hipGetLastError() == hipSuccess ? PAIR_OK : PAIR_EHIP;
 }
 
 int launch_audit_exact(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,

@@ -59,4 +59,18 @@ int launch_audit_exact(int64_t B, int64_t nv, int32_t gmax, const int64_t* offse
                        double* bias_norm, double* gram, void* workspace, int32_t* d_status,
                        hipStream_t stream);
 
+// Gram matrices K_b = S_b S_b^T in fp64 ([B][gmax][gmax], entries beyond G_b
+// not written); the workspace is exact_workspace_bytes(B, gmax, D).
+int launch_gram(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                const void* scores, int64_t ld, double* gram, void* workspace, int32_t* d_status,
+                hipStream_t stream);
+
+size_t direction_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R);
+
+int launch_audit_direction(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                           const void* scores, int64_t ld, const float* rewards, const float* p,
+                           const float* pi_w, int32_t rule, float wmax, uint64_t seed,
+                           int64_t rep0, int64_t R, double* cosine, double* target_norm,
+                           void* workspace, int32_t* d_status, hipStream_t stream);
+
 }  // namespace pair

@@ -153,3 +153,31 @@ def test_rule_entry_points_reject_bad_rules():
 
     assert acall(rule=7) == -1
     assert acall(rule=pair.RULE_CLIPPED, wmax=0.0) == -1
+
+
+def test_audit_direction_rejects_bad_arguments_and_sizes_workspace():
+    L = pair.lib()
+    need = L.pair_audit_direction_workspace_bytes(256, 16, 65536, 4096)
+    assert need > 256 * 4096 * 16 * 4                     # fp32 deviations at least
+    assert L.pair_audit_direction_workspace_bytes(4, 65, 64, 10) == 0
+    assert L.pair_audit_direction_workspace_bytes(4, 8, 64, 0) == 0
+    assert L.pair_audit_direction_workspace_bytes(4, 8, 0, 10) == 0
+    f = L.pair_audit_direction
+
+    def call(dt=1, ws=FAKE, wsb=need, R=4096, gmax=16, cos=FAKE, tn=FAKE, s=FAKE, rule=0,
+             wmax=0.0, rep0=0):
+        return f(256, 4096, gmax, FAKE, 65536, s, dt, 65536, FAKE, FAKE, NULL, rule, wmax, 1, rep0,
+                 R, cos, tn, ws, wsb, NULL, NULL)
+
+    assert call(dt=0) == -2
+    assert call(ws=NULL) == -6
+    assert call(wsb=need - 1) == -6
+    assert call(ws=ctypes.c_void_p((1 << 20) + 16)) == -6
+    assert call(R=0) == -3
+    assert call(rep0=-1) == -3
+    assert call(gmax=80) == -3
+    assert call(cos=NULL) == -1
+    assert call(tn=NULL) == -1
+    assert call(rule=9) == -1
+    assert call(rule=pair.RULE_CLIPPED, wmax=0.0) == -1
+    assert call(s=ODD) == -4
