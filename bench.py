@@ -548,6 +548,86 @@ def time_exact_audit(pair, stream, B, nv, G, off, scores, rew, p, D, reps=10):
                          "algorithmic_bytes": nbytes}}
 
 
+def audit_matrix(pair, stream, wl, dev, R=1000, D=4096):
+    """The frozen-policy audit matrix (App. E; the procedure behind the audit
+    tables of Sec. 5.2) on a synthetic population: the ragged workload's
+    prompt structure (B = 512, G_b ~ U{2..64}), rewards, prefix statistics and
+    suffix lengths, with bf16 N(0, 1/D) scores of width D.  Each row's design
+    is replayed over R draws against the complete-pair target: bias norm and
+    MSE (pair_audit_rule), the mean cosine to the target
+    (pair_audit_direction), and from the same draws (pair_design_inclusion)
+    the completed vertices, observed edges and the suffix tokens spent as a
+    fraction of the full group's.  Bias, MSE and cosine are averaged over the
+    prompts whose target is nonzero, the rest over all prompts."""
+    import numpy as np
+    import torch
+
+    w = wl.WORKLOADS["ragged"].replace(D=D)
+    meta = wl.host_meta(w)
+    inp = wl.alloc_inputs(w, meta.offsets)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    off, rew, ph, ch, bu = (t(a) for a in (meta.offsets, meta.rewards, inp.p_hat, inp.c_hat,
+                                           inp.budget))
+    B, nv, G = meta.B, meta.nv, meta.gmax
+    scores = wl.device_scores(w, nv, dev)
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+    designs = {"full": torch.ones(nv, dtype=torch.float32, device=dev)}
+    with torch.cuda.stream(stream):
+        for name, code in (("pair", pair.DESIGN_PAIR), ("pointwise", pair.DESIGN_POINTWISE),
+                           ("uniform", pair.DESIGN_UNIFORM)):
+            designs[name] = torch.empty(nv, dtype=torch.float32, device=dev)
+            pair.pair_design_alloc(B, nv, G, off, ph, ch, None, bu, 0.08, code, designs[name],
+                                   None, None, st, stream)
+    rows = [("full candidate graph", "full", pair.RULE_HT),
+            ("uniform vertex HT", "uniform", pair.RULE_HT),
+            ("pointwise p(1-p) HT", "pointwise", pair.RULE_HT),
+            ("adaptive unweighted", "pair", pair.RULE_UNWEIGHTED),
+            ("marginal-only weighting", "pair", pair.RULE_MARGINAL),
+            ("PAIR", "pair", pair.RULE_HT)]
+    ws = torch.empty(pair.pair_audit_workspace_bytes(B, G, D, R), dtype=torch.uint8, device=dev)
+    wsd = torch.empty(pair.pair_audit_direction_workspace_bytes(B, G, D, R), dtype=torch.uint8,
+                      device=dev)
+    mse = torch.empty(B, dtype=torch.float64, device=dev)
+    bias = torch.empty(B, dtype=torch.float64, device=dev)
+    cos = torch.empty(B, dtype=torch.float64, device=dev)
+    tnorm = torch.empty(B, dtype=torch.float64, device=dev)
+    mask = torch.empty((R, nv), dtype=torch.uint8, device=dev)
+    ec = torch.empty((R, B), dtype=torch.int32, device=dev)
+    comp = torch.empty((R, B), dtype=torch.int32, device=dev)
+    sizes = torch.from_numpy(np.diff(meta.offsets)).to(dev)
+    owner = torch.repeat_interleave(torch.arange(B, device=dev), sizes)
+    c_tot = torch.zeros(B, dtype=torch.float64, device=dev).index_add_(0, owner, ch.double())
+    seed = w.design_seed
+    out = {"workload": f"ragged structure B={B}, nv={nv}, G_b~U{{2..64}}, D={D} bf16 N(0,1/D), "
+                       f"R={R} draws per design; designs from pair_design_alloc (budget 0.5 sum c, "
+                       f"pi_min 0.08)"}
+    e0, e1 = TimingEvent(), TimingEvent()
+    res = {}
+    with torch.cuda.stream(stream):
+        e0.record(stream)
+        for label, dname, rule in rows:
+            p = designs[dname]
+            pair.pair_audit_rule(B, nv, G, off, scores, rew, p, None, rule, 0.0, seed, 0, R, mse,
+                                 bias, None, None, ws, st, stream)
+            pair.pair_audit_direction(B, nv, G, off, scores, rew, p, None, rule, 0.0, seed, 0, R,
+                                      cos, tnorm, wsd, st, stream)
+            pair.pair_design_inclusion(B, nv, G, off, p, seed, 0, R, mask, None, ec, comp, st,
+                                       stream)
+            cost = torch.zeros((R, B), dtype=torch.float64, device=dev).index_add_(
+                1, owner, mask.double() * ch.double()[None, :]) / c_tot[None, :]
+            live = tnorm > 0
+            res[label] = {"bias": bias[live].mean(), "mse": mse[live].mean(), "cosine": cos[live].mean(),
+                          "vertices": comp.double().mean(), "edges": ec.double().mean(),
+                          "suffix_tokens": cost.mean()}
+        e1.record(stream)
+    torch.cuda.synchronize()
+    if int(st.item()) != 0:
+        raise RuntimeError(f"device status {int(st.item())} in the audit matrix")
+    out["ms"] = round(e0.elapsed_time(e1), 3)
+    out["rows"] = {k: {m: round(float(v.item()), 6) for m, v in r.items()} for k, r in res.items()}
+    return out
+
+
 def time_variants(pair, stream, B, nv, G, off, rew, mask, pi, coeff, audit_args, status, reps=5):
     """Estimator variants (edge-weight rules): the coefficient fold on the
     b128 draw and the audit replay on the audit workload, per rule, timed
@@ -798,6 +878,7 @@ def main():
     result["variants"] = time_variants(pair, stream, B, nv, G, off, rew, mask, pi, coeff,
                                        (Ba, nva, Ga, off_a, scores_a, rew_a, p_a, wa, R, mse, bias,
                                         reps, ec_a, ws), status)
+    result["audit_matrix"] = audit_matrix(pair, stream, wl, dev)
     if not args.no_cpu_baseline:
         _log("[bench] timing the CPU oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(meta, w, scores, meta_a, wa, scores_a)
