@@ -210,7 +210,7 @@ def test_random_rule_coefficients_and_gradient(case_id):
     assert err <= (BF16_TOL if c["bf16"] else FP32_TOL)
 
 
-@pytest.mark.parametrize("case_id", range(6))
+@pytest.mark.parametrize("case_id", range(12))
 def test_random_rule_audit(case_id):
     rng = np.random.default_rng(9700 + case_id)
     c = _case(rng, 4, (33, 500, 2049), bf16=True)
@@ -234,6 +234,19 @@ def test_random_rule_audit(case_id):
     b_err = np.max(np.abs(bias - want["bias_norm"]) / np.maximum(want["bias_norm"], 1e-300))
     log(f"  rep_sqerr rel L2 {e_err:.2e}, max mse rel {m_err:.2e}, max bias rel {b_err:.2e}")
     assert e_err <= BF16_TOL and m_err <= BF16_TOL and b_err <= BF16_TOL
+    # The update-direction column of the same replicates.
+    dirn = pair.audit_direction(off, c["dev"], torch.from_numpy(c["rewards"]).to(DEV),
+                                torch.from_numpy(c["p"]).to(DEV), c["seed"], c["rep0"], R, gmax,
+                                rule=rule, wmax=wmax, nv=nv)
+    torch.cuda.synchronize()
+    assert int(dirn["status"].item()) == 0
+    cos, tn = dirn["cosine"].cpu().numpy(), dirn["target_norm"].cpu().numpy()
+    live = want["target_norm"] > 0
+    assert np.all(cos[~live] == 0.0) and np.all(tn[~live] == 0.0)
+    c_err = float(np.max(np.abs(cos - want["cosine"])))
+    t_err = float(np.max(np.abs(tn[live] / want["target_norm"][live] - 1.0))) if live.any() else 0.0
+    log(f"  cosine max abs {c_err:.2e}, target norm max rel {t_err:.2e}")
+    assert c_err <= 1e-5 and t_err <= 1e-5
 
 
 @pytest.mark.parametrize("case_id", range(8))
