@@ -364,8 +364,14 @@ class TimingEvent:
         return float(ms.value)
 
     def __del__(self):
-        if self._hip is not None and self.h:
+        # At interpreter exit the HIP runtime may already be torn down; the
+        # process ends anyway, so the event is left to it.
+        if sys.is_finalizing() or self._hip is None or not self.h:
+            return
+        try:
             self._hip.hipEventDestroy(self.h)
+        except Exception:
+            pass
 
 
 def _event_ms(stream, fn, reps):
