@@ -280,6 +280,6 @@ const char* pair_strerror(int code) {
   }
 }
 
-int pair_version(void) { return 100; }
+int pair_version(void) { return 200; }   // 0.2.0: pair_audit_direction added
 
 }  // extern "C"
