@@ -17,7 +17,11 @@ Parity status of each function (what pins it, see ``tests/test_oracle_pins.py``)
                     p == 1 gives (r_i - mean r)/(G - 1)
   audit             pinned: exact design covariance trace (Prop 1) by
                     enumeration; Gram-matrix identity for every replicate;
-                    bias^2 ~ MSE/R statistics; p == 1 gives zero MSE
+                    bias^2 ~ MSE/R statistics; p == 1 gives zero MSE;
+                    cosine to the target: the Gram identity over the
+                    coefficients per replicate, 1 when p == 1, the fraction of
+                    draws with both candidates when G == 2, 0 for equal
+                    rewards, invariant to rescaled scores and rewards
   audit_exact       pinned: exhaustive design enumeration of E||g^ - t||^2 and
                     of the mean for every linear rule; zero bias for HT
                     (Thm 2); Prop. 1's unweighted bias vector; zero error
@@ -26,7 +30,9 @@ Parity status of each function (what pins it, see ``tests/test_oracle_pins.py``)
                     probabilities pinned by brute force over every sample;
                     the sequential draw's sample probabilities pinned to
                     prod w / e_n by walking every path; the fit's output
-                    reproduces its target; draw frequencies vs pi and pi_ij
+                    reproduces its target and returns odds of geometric mean
+                    1 (also when the start already meets the target); draw
+                    frequencies vs pi and pi_ij
   *_rule variants   pinned by exhaustive design enumeration against the
                     expectations the paper states for each edge-weight rule
                     (naive bias, clipped multiplier min(1, w_max rho) - 1,
