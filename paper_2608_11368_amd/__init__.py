@@ -340,6 +340,27 @@ def design_inclusion(offsets, p, seed, rep0, R, gmax, want_mask=True, want_pi=Tr
     return out
 
 
+def design_coeffs(offsets, p, rewards, seed, rep, gmax, want_mask=True, want_pi=True, nv=None,
+                  stream=None):
+    """One replicate's design draw and its sequence advantages A~ in one
+    launch (the per-rollout weights a trainer applies to the log-probability
+    gradients), with the mask and the logged rho block."""
+    B = offsets.numel() - 1
+    nv = _nv(offsets) if nv is None else nv
+    dev = p.device
+    out = {
+        "coeff": torch.empty(nv, dtype=torch.float32, device=dev),
+        "mask": torch.empty(nv, dtype=torch.uint8, device=dev) if want_mask else None,
+        "pi": torch.empty((B, gmax, gmax), dtype=torch.float32, device=dev) if want_pi else None,
+        "edge_count": torch.empty(B, dtype=torch.int32, device=dev),
+        "completed": torch.empty(B, dtype=torch.int32, device=dev),
+        "status": torch.zeros(1, dtype=torch.int32, device=dev),
+    }
+    pair_design_coeffs(B, nv, gmax, offsets, p, rewards, seed, rep, out["coeff"], out["mask"],
+                       out["pi"], out["edge_count"], out["completed"], out["status"], stream)
+    return out
+
+
 def edge_coeffs(offsets, rewards, mask, pi, gmax, nv=None, rule=None, wmax=0.0, stream=None):
     """Coefficients; with `rule` (RULE_*) also returns the ESS and the maximum weight."""
     B = offsets.numel() - 1

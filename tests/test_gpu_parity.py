@@ -277,6 +277,12 @@ def test_fused_design_coeffs_is_bitwise_the_two_calls(name, B):
     assert torch.equal(ec, d["edge_count"][0]) and torch.equal(comp, d["completed"][0])
     od = oracle.design_inclusion(meta.offsets, meta.p, w.design_seed, 3, 1, meta.gmax)
     assert np.array_equal(mask.cpu().numpy(), od["mask"][0])
+    h = pair.design_coeffs(dm["offsets"], dm["p"], dm["rewards"], w.design_seed, 3, meta.gmax,
+                           nv=meta.nv)
+    torch.cuda.synchronize()
+    assert int(h["status"].item()) == 0
+    assert torch.equal(h["coeff"], coeff) and torch.equal(h["mask"], mask)
+    assert torch.equal(h["pi"], pi) and torch.equal(h["edge_count"], ec)
 
 
 # ------------------------------------------- weighted gradient, batch mean --
