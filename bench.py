@@ -737,7 +737,7 @@ def main():
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one MI355X: this build runs on a single GPU "
+        print("bench.py measures one MI355X: the library runs on a single GPU "
               "(no collectives); run it with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
