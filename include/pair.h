@@ -6,7 +6,7 @@
  * ---------------------------------------
  *  - Every array argument is a DEVICE pointer owned by the caller.  The library
  *    never allocates, frees or retains caller memory; scratch space is passed
- *    in explicitly (pair_audit's workspace).
+ *    in explicitly (the audits' workspaces).
  *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *    All work is enqueued asynchronously on it; nothing blocks the host.
  *  - Host-detectable argument errors return a negative PAIR_E* code and

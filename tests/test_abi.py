@@ -181,3 +181,37 @@ def test_audit_direction_rejects_bad_arguments_and_sizes_workspace():
     assert call(rule=9) == -1
     assert call(rule=pair.RULE_CLIPPED, wmax=0.0) == -1
     assert call(s=ODD) == -4
+
+
+def test_header_is_plain_c_and_links_from_a_c_caller(tmp_path):
+    """include/pair.h compiles as strict C99 and as C++11, and a C program
+    linked against libpair.so runs the host-side entry points (no GPU: the
+    calls it makes return before touching the device)."""
+    prog = tmp_path / "caller.c"
+    prog.write_text(r'''
+#include <stdio.h>
+#include <string.h>
+#include "pair.h"
+int main(void) {
+  if (pair_version() < 100) return 1;
+  if (strcmp(pair_strerror(PAIR_OK), "ok") != 0) return 2;
+  /* argument checks happen before any device work */
+  if (pair_weighted_grad(4, 32, NULL, 64, NULL, PAIR_BF16, 64, NULL, NULL, 0, NULL, NULL) !=
+      PAIR_EINVAL) return 3;
+  if (pair_audit_workspace_bytes(4, 65, 64, 10) != 0) return 4;
+  printf("c caller ok %d\n", pair_version());
+  return 0;
+}
+''')
+    inc = os.path.join(ROOT, "include")
+    for cmd in (["gcc", "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic", "-fsyntax-only"],
+                ["g++", "-std=c++11", "-Wall", "-Wextra", "-Werror", "-fsyntax-only", "-x", "c++"]):
+        subprocess.run(cmd + ["-I", inc, str(prog)], check=True, capture_output=True)
+    libdir = os.path.dirname(pair.LIB_PATH)
+    exe = tmp_path / "caller"
+    subprocess.run(["gcc", "-std=c99", "-I", inc, str(prog), "-o", str(exe), "-L", libdir,
+                    "-l:" + os.path.basename(pair.LIB_PATH), f"-Wl,-rpath,{libdir}",
+                    "-Wl,-rpath-link,/opt/rocm/lib"], check=True, capture_output=True)
+    res = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert "c caller ok" in res.stdout
