@@ -16,8 +16,9 @@
 //                   table W_ij = (r_i - r_j)/rho_ij in LDS, centring over the
 //                   completed vertices, delta_r stored in fp32, and a
 //                   fixed-order partial sum of delta over the 256 lanes.
-//  2. audit_prep    delta_bar appended as replicate row R, padding rows
-//                   zeroed.
+//  2. audit_prep    replicate rows padded with zero rows to a whole number
+//                   of tile pairs (R rounded up to 64), delta_bar stored
+//                   as the first row of one more tile, the rest zeroed.
 //  3. audit_mfma    the contraction on v_mfma_f32_32x32x16_f16.  Each score
 //                   row of a column slice is rescaled by 2^-e_i, with e_i
 //                   the exponent of the row's largest magnitude within the
@@ -36,7 +37,8 @@
 //                   delta rows are shared through that XCD's L2.
 //  4. audit_sqerr   e_r = per-slice partial sums reduced in fixed order, one
 //                   thread per (prompt, replicate); fp64 partial sums of e_r
-//     audit_final   per prompt: MSE = fp64 mean of e_r, bias = sqrt(e[R]).
+//     audit_final   per prompt: MSE = fp64 mean of e_r, bias = sqrt(e of the
+//                   delta_bar row).
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -64,7 +66,8 @@ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 struct AuditLayout {
   int ks;            // 16-wide K steps (ceil(gmax / 16))
   int kp;            // 16 * ks: padded K extent
-  int64_t ntiles;    // 32-row replicate tiles per prompt (R rows + the delta_bar row)
+  int64_t rbar;      // the delta_bar row: R rounded up to whole pairs of tiles
+  int64_t ntiles;    // 32-row tiles per prompt: rbar / 32 replicate tiles + the delta_bar tile
   int64_t rrows;     // ntiles * 32
   int64_t nslices;   // score-column slices per prompt
   int64_t nwg;       // audit_coeffs workgroups per prompt
@@ -76,7 +79,8 @@ AuditLayout audit_layout(int64_t B, int32_t gmax, int64_t D, int64_t R) {
   AuditLayout L;
   L.ks = (gmax + 15) / 16;
   L.kp = 16 * L.ks;
-  L.ntiles = (R + 1 + kTile - 1) / kTile;
+  L.rbar = round_up(R, (int64_t)kPair * kTile);
+  L.ntiles = L.rbar / kTile + 1;
   L.rrows = L.ntiles * kTile;
   L.nslices = (D + slice_cols(L.ks) - 1) / slice_cols(L.ks);
   L.nwg = (R + kCoefThreads - 1) / kCoefThreads;
@@ -278,7 +282,8 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void audit_prep_kernel(int64_t B, int64_t nv, int32_t gmax, int kp,
                                                          const int64_t* __restrict__ offsets,
-                                                         int64_t R, int64_t nwg, int64_t rrows,
+                                                         int64_t R, int64_t rbar, int64_t nwg,
+                                                         int64_t rrows,
                                                          const float* __restrict__ dsum,
                                                          float* __restrict__ delta) {
   const int64_t b = blockIdx.x;
@@ -292,11 +297,16 @@ __global__ __launch_bounds__(256) void audit_prep_kernel(int64_t B, int64_t nv, 
       for (int64_t c = 0; c < nwg; ++c) s += dsum[(b * nwg + c) * gmax + tid];
       v = s / (float)R;
     }
-    delta[(b * rrows + R) * kp + tid] = v;
+    delta[(b * rrows + rbar) * kp + tid] = v;
   }
-  const int64_t pad = (rrows - R - 1) * kp;
-  float* dst = delta + (b * rrows + R + 1) * kp;
-  for (int64_t idx = tid; idx < pad; idx += blockDim.x) dst[idx] = 0.0f;
+  // Zero rows: R .. rbar-1 (padding of the replicate tiles) and the rest of
+  // the delta_bar tile.
+  const int64_t pad1 = (rbar - R) * kp;
+  float* dst1 = delta + (b * rrows + R) * kp;
+  for (int64_t idx = tid; idx < pad1; idx += blockDim.x) dst1[idx] = 0.0f;
+  const int64_t pad2 = (rrows - rbar - 1) * kp;
+  float* dst2 = delta + (b * rrows + rbar + 1) * kp;
+  for (int64_t idx = tid; idx < pad2; idx += blockDim.x) dst2[idx] = 0.0f;
 }
 
 // ---------------------------------------------------------------------------
@@ -531,10 +541,12 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
   };
 
   float* eo = epart + (b * nslices + sl) * rrows;
-  // Main tiles in pairs, round-robin over the waves; the tiles left over
-  // (fewer than one pair per wave) are split by steps across all waves.
+  // Replicate tiles (an even count) in pairs, round-robin over the waves, so
+  // every replicate's partial is formed the same way whatever R and the first
+  // replicate index; the last tile (delta_bar) is split by steps across all
+  // waves.
   const int64_t per_round = (int64_t)kPair * kMfmaWaves;
-  const int64_t nmain = ntiles / per_round * per_round;
+  const int64_t nmain = ntiles - 1;
   for (int64_t t0 = (int64_t)wave * kPair; t0 < nmain; t0 += per_round) {
     f16x8_t Bt[kPair][KS];
     int fr[kPair];
@@ -573,7 +585,7 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kSqThreads) void audit_sqerr_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets, int64_t R,
-    int64_t rrows, int64_t nslices, int64_t nsq, const float* __restrict__ epart,
+    int64_t rbar, int64_t rrows, int64_t nslices, int64_t nsq, const float* __restrict__ epart,
     double* __restrict__ rpart, float* __restrict__ ebar, float* __restrict__ rep_sqerr) {
   __shared__ double part[kSqThreads / kWave];
   const int64_t b = blockIdx.x / nsq;
@@ -583,7 +595,7 @@ __global__ __launch_bounds__(kSqThreads) void audit_sqerr_kernel(
   const int64_t r = c * kSqThreads + threadIdx.x;
   float e = 0.0f;
   if (r <= R) {
-    const float* eb = epart + b * nslices * rrows + r;
+    const float* eb = epart + b * nslices * rrows + (r < R ? r : rbar);
     int64_t k = 0;
     for (; k + 8 <= nslices; k += 8) {
       float v[8];
@@ -838,7 +850,7 @@ int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, in
   if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
 
   hipLaunchKernelGGL(audit_prep_kernel, dim3((unsigned)B), dim3(256), 0, stream, B, nv, gmax, L.kp,
-                     offsets, R, L.nwg, L.rrows, dsum, delta);
+                     offsets, R, L.rbar, L.nwg, L.rrows, dsum, delta);
   if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
 
   const int64_t grid = round_up(B * L.nslices, 8);
@@ -859,7 +871,7 @@ int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, in
   const int64_t sq_grid = B * L.nsq;
   if (sq_grid > 0x7fffffffLL) return PAIR_ERANGE;
   hipLaunchKernelGGL(audit_sqerr_kernel, dim3((unsigned)sq_grid), dim3(kSqThreads), 0, stream, B,
-                     nv, gmax, offsets, R, L.rrows, L.nslices, L.nsq, epart, rpart, ebar,
+                     nv, gmax, offsets, R, L.rbar, L.rrows, L.nslices, L.nsq, epart, rpart, ebar,
                      rep_sqerr);
   if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
   hipLaunchKernelGGL(audit_final_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, stream,

@@ -157,3 +157,41 @@ def test_full_size_exact_audit_and_monte_carlo_consistency():
     assert abs(z.mean()) <= 4.0 / np.sqrt(live.sum()) + 0.05 and np.abs(z).max() <= 5.5
     del sd
     torch.cuda.empty_cache()
+
+
+def test_audit_at_the_papers_fifty_thousand_draws():
+    """The Monte-Carlo audit at the paper's draw count (R = 50,000; Sec. 5.2)
+    on 64 prompts of the audit workload at full width: every prompt's MSE
+    within 5 standard errors of its exact Prop. 1 value, the bias norm of the
+    unbiased HT estimator at the sqrt(MSE / R) scale, and the replicate range
+    split into two calls equal to one call."""
+    w = wl.WORKLOADS["audit"].replace(B=64)
+    meta = wl.host_meta(w)
+    R = 50000
+    log(f"audit at R={R}: B={meta.B} D={w.D}")
+    dm = upload_meta(meta)
+    sd = wl.device_scores(w, meta.nv, DEV)
+    ex = pair.audit_exact(dm["offsets"], sd, dm["rewards"], dm["p"], meta.gmax, nv=meta.nv)
+    mc = pair.audit(dm["offsets"], sd, dm["rewards"], dm["p"], w.design_seed, 0, R, meta.gmax,
+                    nv=meta.nv)
+    half = pair.audit(dm["offsets"], sd, dm["rewards"], dm["p"], w.design_seed, R // 2, R // 2,
+                      meta.gmax, nv=meta.nv)
+    torch.cuda.synchronize()
+    assert int(ex["status"].item()) == 0 and int(mc["status"].item()) == 0
+    e_mse, m_mse = ex["mse"].cpu().numpy(), mc["mse"].cpu().numpy()
+    reps = mc["rep_sqerr"].cpu().numpy().astype(np.float64)
+    live = e_mse > 0
+    se = reps.std(axis=1) / np.sqrt(R)
+    z = (m_mse[live] - e_mse[live]) / se[live]
+    bias = mc["bias_norm"].cpu().numpy()
+    ratio = bias[live] / np.sqrt(e_mse[live] / R)
+    log(f"  z over {live.sum()} prompts: mean {z.mean():+.3f}, max |z| {np.abs(z).max():.2f}; "
+        f"bias / sqrt(MSE/R): median {np.median(ratio):.2f}, max {ratio.max():.2f}")
+    assert np.all(m_mse[~live] == 0.0)
+    assert np.abs(z).max() <= 5.0 and abs(z.mean()) <= 4.0 / np.sqrt(live.sum()) + 0.05
+    # E||mean_r g_r - t||^2 = MSE / R for HT (Theorem 2): the ratio is a
+    # chi-like variable of order 1.
+    assert np.median(ratio) <= 2.0 and ratio.max() <= 6.0
+    assert torch.equal(half["rep_sqerr"], mc["rep_sqerr"][:, R // 2:])
+    del sd
+    torch.cuda.empty_cache()
