@@ -30,6 +30,7 @@ import ctypes
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -48,11 +49,21 @@ def _log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+_C_TOKENS = re.compile(r'//[^\n]*|/\*.*?\*/|"(?:\\.|[^"\\\n])*"|\'(?:\\.|[^\'\\\n])*\'', re.S)
+
+
+def _code_only(text):
+    """C++ source with comments removed and whitespace runs collapsed, so that
+    editing a comment does not count as a change of the kernel."""
+    text = _C_TOKENS.sub(lambda m: m.group(0) if m.group(0)[0] in "\"'" else " ", text)
+    return " ".join(text.split())
+
+
 def _source_sha(*names):
     h = hashlib.sha256()
     for n in names:
-        with open(os.path.join(ROOT, "paper_2608_11368_amd", "csrc", n), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2608_11368_amd", "csrc", n), encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 

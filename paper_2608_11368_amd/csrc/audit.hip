@@ -18,7 +18,7 @@
 //                   fixed-order partial sum of delta over the 256 lanes.
 //  2. audit_prep    replicate rows padded with zero rows to a whole number
 //                   of tile pairs (R rounded up to 64), delta_bar stored
-//                   as the first row of one more tile, the rest zeroed.
+//                   in the row after them.
 //  3. audit_mfma    the contraction on v_mfma_f32_32x32x16_f16.  Each score
 //                   row of a column slice is rescaled by 2^-e_i, with e_i
 //                   the exponent of the row's largest magnitude within the
@@ -34,7 +34,9 @@
 //                   once; the squares of every output tile are summed in the
 //                   epilogue and the rows x D product is never written.
 //                   Workgroups of one prompt are placed on one XCD so its
-//                   delta rows are shared through that XCD's L2.
+//                   delta rows are shared through that XCD's L2.  The
+//                   delta_bar row is one fp32 dot product per score column
+//                   on the vector units against the same LDS slice.
 //  4. audit_sqerr   e_r = per-slice partial sums reduced in fixed order, one
 //                   thread per (prompt, replicate); fp64 partial sums of e_r
 //     audit_final   per prompt: MSE = fp64 mean of e_r, bias = sqrt(e of the
@@ -339,9 +341,12 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
   constexpr int kPieces = KP * (SW / 8);    // 16-byte pieces of the slice
   constexpr int kPerThread = (kPieces + kMfmaThreads - 1) / kMfmaThreads;
   __shared__ __align__(16) uint16_t S_lds[kRowsLds * KP];
-  __shared__ float tail_part[kMfmaWaves][kTile];
+  __shared__ float bar_part[kMfmaWaves];
+  __shared__ float wbar[KP];
+  __shared__ int fbar;
   __shared__ uint32_t row_max[KP];
   __shared__ int32_t ex[KP];
+  static_assert(kSteps % 2 == 0 && SW % kMfmaThreads == 0 && KP <= kWave, "slice shape");
 
   // XCD-aware placement: hardware round-robins workgroup ids over 8 XCDs;
   // give each XCD a contiguous range of logical (prompt, slice) ids so the
@@ -414,15 +419,29 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
     if (cur >= 0 && m != 0u) atomicMax(&row_max[cur], m);
   }
   __syncthreads();
-  if (tid < KP) {
-    const uint32_t mm = row_max[tid];
-    int32_t e = 0;
-    if (mm >= 0x7f80u) {                 // inf or NaN in the row
-      raise_status(d_status, PAIR_ST_NONFINITE);
-    } else if (mm != 0u) {
-      e = (int32_t)(mm >> 7) - 127;      // -127 for a row of subnormals
+  // Per-row exponents, and the delta_bar row rescaled like a replicate row:
+  // w_i = delta_bar_i 2^(e_i - f) with f putting the largest entry in [1, 2).
+  // The first wave holds all KP rows; its shuffles run on every lane.
+  const float* dbar = delta + (b * rrows + (ntiles - 1) * kTile) * KP;
+  if (wave == 0) {
+    float y = 0.0f;
+    if (lane < KP) {
+      const uint32_t mm = row_max[lane];
+      int32_t e = 0;
+      if (mm >= 0x7f80u) {               // inf or NaN in the row
+        raise_status(d_status, PAIR_ST_NONFINITE);
+      } else if (mm != 0u) {
+        e = (int32_t)(mm >> 7) - 127;    // -127 for a row of subnormals
+      }
+      ex[lane] = e;
+      y = ldexpf(dbar[lane], e);
     }
-    ex[tid] = e;
+    float m = fabsf(y);
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+    const int f = m > 0.0f ? ilogbf(m) : 0;
+    if (lane < KP) wbar[lane] = ldexpf(y, -f);
+    if (lane == 0) fbar = f;
   }
   __syncthreads();
 #pragma unroll
@@ -482,9 +501,9 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
       for (int j = 0; j < 8; ++j) Bf[s][j] = (_Float16)ldexpf(y[s][j], -f);
   };
 
-  // Sweep `np` tiles (np <= kPair) over steps [s0, s1); returns each tile's
+  // Sweep a pair of tiles over all steps of the slice; returns each tile's
   // sum of squares for replicate row l % 32 (lanes l and l + 32 combined).
-  auto sweep = [&](const f16x8_t (&Bt)[kPair][KS], int np, int s0, int s1, float (&out)[kPair]) {
+  auto sweep = [&](const f16x8_t (&Bt)[kPair][KS], float (&out)[kPair]) {
     f32x16_t accA[kPair], accB[kPair];
     float sq[kPair][4];
 #pragma unroll
@@ -497,38 +516,28 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
     auto step = [&](const f16x8_t (&Af)[KS], f32x16_t (&acc)[kPair], const f32x16_t (&prev)[kPair]) {
 #pragma unroll
       for (int q = 0; q < kPair; ++q) {
-        if (q < np) {
-          f32x16_t a;
+        f32x16_t a;
 #pragma unroll
-          for (int v = 0; v < 16; ++v) a[v] = 0.0f;
+        for (int v = 0; v < 16; ++v) a[v] = 0.0f;
 #pragma unroll
-          for (int s = 0; s < KS; ++s)
-            a = __builtin_amdgcn_mfma_f32_32x32x16_f16(Af[s], Bt[q][s], a, 0, 0, 0);
-          acc[q] = a;
+        for (int s = 0; s < KS; ++s)
+          a = __builtin_amdgcn_mfma_f32_32x32x16_f16(Af[s], Bt[q][s], a, 0, 0, 0);
+        acc[q] = a;
 #pragma unroll
-          for (int v = 0; v < 16; ++v)
-            sq[q][v & 3] = __builtin_fmaf(prev[q][v], prev[q][v], sq[q][v & 3]);
-          __builtin_amdgcn_sched_group_barrier(0x008, KS, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
-        }
+        for (int v = 0; v < 16; ++v)
+          sq[q][v & 3] = __builtin_fmaf(prev[q][v], prev[q][v], sq[q][v & 3]);
+        __builtin_amdgcn_sched_group_barrier(0x008, KS, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
     };
     f16x8_t A0[KS], A1[KS];
-    int st = s0;
-    if (st < s1) read_a(st, A0);
-    for (; st + 1 < s1; st += 2) {
+    read_a(0, A0);
+    for (int st = 0; st < kSteps; st += 2) {
       read_a(st + 1, A1);
       step(A0, accA, accB);
-      if (st + 2 < s1) read_a(st + 2, A0);
+      if (st + 2 < kSteps) read_a(st + 2, A0);
       step(A1, accB, accA);
-    }
-    if (st < s1) {            // odd step count: one more step into accA
-      step(A0, accA, accB);
-#pragma unroll
-      for (int q = 0; q < kPair; ++q)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) accB[q][v] = accA[q][v];
     }
 #pragma unroll
     for (int q = 0; q < kPair; ++q) {
@@ -540,11 +549,40 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
     }
   };
 
+  // The delta_bar row on the vector units: one dot product per score column
+  // of the slice (KP FMAs against the fp16 slice in LDS), squares summed per
+  // thread, then over the wave and the waves in a fixed order.  It is one row
+  // against the slice's 2 x (R rounded up to 64) replicate-row sweeps.
+  {
+    float bsq = 0.0f;
+    for (int c = tid; c < SW; c += kMfmaThreads) {
+      const int cl = c % kTile;
+      const uint16_t* src = &S_lds[(c / kTile) * (kTile + kTile / 8) * KP + (cl + cl / 8) * KP];
+      float y = 0.0f;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const uint4 h0 = *reinterpret_cast<const uint4*>(src + 16 * s);
+        const uint4 h1 = *reinterpret_cast<const uint4*>(src + 16 * s + 8);
+        const uint32_t hw[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float lo = (float)__builtin_bit_cast(_Float16, (uint16_t)(hw[j] & 0xffffu));
+          const float hi = (float)__builtin_bit_cast(_Float16, (uint16_t)(hw[j] >> 16));
+          y = __builtin_fmaf(wbar[16 * s + 2 * j], lo, y);
+          y = __builtin_fmaf(wbar[16 * s + 2 * j + 1], hi, y);
+        }
+      }
+      bsq = __builtin_fmaf(y, y, bsq);
+    }
+#pragma unroll
+    for (int o = kWave / 2; o >= 1; o >>= 1) bsq += __shfl_xor(bsq, o, kWave);
+    if (lane == 0) bar_part[wave] = bsq;
+  }
+
   float* eo = epart + (b * nslices + sl) * rrows;
   // Replicate tiles (an even count) in pairs, round-robin over the waves, so
   // every replicate's partial is formed the same way whatever R and the first
-  // replicate index; the last tile (delta_bar) is split by steps across all
-  // waves.
+  // replicate index.
   const int64_t per_round = (int64_t)kPair * kMfmaWaves;
   const int64_t nmain = ntiles - 1;
   for (int64_t t0 = (int64_t)wave * kPair; t0 < nmain; t0 += per_round) {
@@ -553,27 +591,17 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
 #pragma unroll
     for (int q = 0; q < kPair; ++q) load_b(t0 + q, Bt[q], fr[q]);
     float out[kPair];
-    sweep(Bt, kPair, 0, kSteps, out);
+    sweep(Bt, out);
     if (lane < kTile) {
 #pragma unroll
       for (int q = 0; q < kPair; ++q) eo[(t0 + q) * kTile + lane] = ldexpf(out[q], 2 * fr[q]);
     }
   }
-  for (int64_t t = nmain; t < ntiles; ++t) {
-    f16x8_t Bt[kPair][KS];
-    int fr[kPair];
-    load_b(t, Bt[0], fr[0]);
-    const int s0 = wave * kSteps / kMfmaWaves, s1 = (wave + 1) * kSteps / kMfmaWaves;
-    float out[kPair];
-    sweep(Bt, 1, s0, s1, out);
-    if (lane < kTile) tail_part[wave][lane] = out[0];
-    __syncthreads();
-    if (wave == 0 && lane < kTile) {
-      float tot = 0.0f;
-      for (int w = 0; w < kMfmaWaves; ++w) tot += tail_part[w][lane];
-      eo[t * kTile + lane] = ldexpf(tot, 2 * fr[0]);
-    }
-    __syncthreads();
+  __syncthreads();
+  if (tid == 0) {
+    float tot = 0.0f;
+    for (int w = 0; w < kMfmaWaves; ++w) tot += bar_part[w];
+    eo[nmain * kTile] = ldexpf(tot, 2 * fbar);
   }
 }
 
