@@ -327,9 +327,12 @@ size_t pair_audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R)
  * are fp16 after exact power-of-two rescaling (score rows by their largest
  * magnitude, which makes the bf16 -> fp16 conversion exact; each replicate
  * row of A~^(r) - a by its largest entry, then one fp16 rounding), so e_r
- * carries a relative error of about 2^-11 per coefficient.  Weights use
- * rho = pi_w when given (e.g. all ones replays the unweighted estimator of
- * Prop. 1), else the logged fl32(p_i p_j).
+ * carries a relative error of about 2^-11 per coefficient.  The bias row
+ * (1/R) sum_r (A~^(r) - a) is applied in fp32 on the vector units, without
+ * that rounding.  A replicate's e_r does not depend on R or rep0: calls over
+ * consecutive replicate ranges return bitwise the rep_sqerr of one call over
+ * their union.  Weights use rho = pi_w when given (e.g. all ones replays the
+ * unweighted estimator of Prop. 1), else the logged fl32(p_i p_j).
  *
  *   scores, dtype  PAIR_BF16 only, finite values
  *   rewards, p     fp32 [nv]

@@ -609,7 +609,7 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
 // 4. Fixed-order reductions.  audit_sqerr: one thread per (prompt, replicate
 //    row) sums the per-slice partials in slice order (fp32) into e_r, and
 //    each workgroup writes the fp64 sum of its e_r; audit_final: per prompt,
-//    MSE = (sum of those partials in order) / R and bias = sqrt(e_R).
+//    MSE = (sum of those partials in order) / R and bias = sqrt(e of delta_bar).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kSqThreads) void audit_sqerr_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets, int64_t R,
