@@ -136,11 +136,11 @@ def test_random_gradient_chain(case_id):
     assert np.isfinite(gm).all() and rel_l2(gm, est.mean(axis=0)) <= tol
 
 
-@pytest.mark.parametrize("case_id", range(10))
+@pytest.mark.parametrize("case_id", range(16))
 def test_random_audit(case_id):
     rng = np.random.default_rng(9100 + case_id)
     c = _case(rng, 5, (1, 33, 500, 2047, 2049, 3000), bf16=True)
-    R = int(rng.choice([1, 31, 32, 33, 100]))
+    R = int(rng.choice([1, 31, 32, 33, 63, 64, 65, 100, 129]))
     B, nv, gmax = c["B"], c["nv"], c["gmax"]
     log(f"random audit {case_id}: B={B} nv={nv} gmax={gmax} D={c['D']} ld={c['ld']} R={R} "
         f"rep0={c['rep0']}")
@@ -216,7 +216,7 @@ def test_random_rule_audit(case_id):
     c = _case(rng, 4, (33, 500, 2049), bf16=True)
     rule = RULES[case_id % len(RULES)]
     wmax = _wmax(rng, rule)
-    R = int(rng.choice([31, 64]))
+    R = int(rng.choice([31, 64, 65, 129]))
     B, nv, gmax = c["B"], c["nv"], c["gmax"]
     log(f"random rule audit {rule} case {case_id}: B={B} gmax={gmax} D={c['D']} R={R}")
     off = torch.from_numpy(c["offsets"]).to(DEV)
