@@ -9,8 +9,9 @@ audit, every edge-weight rule (coefficients, ESS, maximum weight, gradient,
 audit replay) and the exact audit of the linear rules.  The bars are those of
 the parity tests: masks, logged rho and counts bit-exact; coefficients and fp32
 gradients within 1e-5 relative L2, bf16 gradients within 2e-3; exact zeros
-where the oracle's estimate is exactly zero; audit MSE, bias norm and
-per-replicate squared errors within 2e-3 relative, edge counts bit-exact.
+where the oracle's estimate is exactly zero; audit MSE and per-replicate
+squared errors within 2e-3 relative, the bias norm (its row applied in fp32)
+within 5e-5, edge counts bit-exact.
 """
 import numpy as np
 import pytest
@@ -24,6 +25,7 @@ pytestmark = pytest.mark.gpu
 
 FP32_TOL = 1e-5
 BF16_TOL = 2e-3
+BIAS_TOL = 5e-5
 WIDTHS = (1, 2, 7, 31, 255, 1000, 1023, 1025, 2047, 2049, 4095, 4097, 6000)
 
 
@@ -157,7 +159,7 @@ def test_random_audit(case_id):
     m_err = np.max(np.abs(mse - want["mse"]) / np.maximum(want["mse"], 1e-300))
     b_err = np.max(np.abs(bias - want["bias_norm"]) / np.maximum(want["bias_norm"], 1e-300))
     log(f"  rep_sqerr rel L2 {e_err:.2e}, max mse rel {m_err:.2e}, max bias rel {b_err:.2e}")
-    assert e_err <= BF16_TOL and m_err <= BF16_TOL and b_err <= BF16_TOL
+    assert e_err <= BF16_TOL and m_err <= BF16_TOL and b_err <= BIAS_TOL
 
 
 RULES = [pair.RULE_HT, pair.RULE_UNWEIGHTED, pair.RULE_RATIO_KE, pair.RULE_CLIPPED,
@@ -233,7 +235,7 @@ def test_random_rule_audit(case_id):
     m_err = np.max(np.abs(mse - want["mse"]) / np.maximum(want["mse"], 1e-300))
     b_err = np.max(np.abs(bias - want["bias_norm"]) / np.maximum(want["bias_norm"], 1e-300))
     log(f"  rep_sqerr rel L2 {e_err:.2e}, max mse rel {m_err:.2e}, max bias rel {b_err:.2e}")
-    assert e_err <= BF16_TOL and m_err <= BF16_TOL and b_err <= BF16_TOL
+    assert e_err <= BF16_TOL and m_err <= BF16_TOL and b_err <= BIAS_TOL
     # The update-direction column of the same replicates.
     dirn = pair.audit_direction(off, c["dev"], torch.from_numpy(c["rewards"]).to(DEV),
                                 torch.from_numpy(c["p"]).to(DEV), c["seed"], c["rep0"], R, gmax,
