@@ -21,6 +21,7 @@ on the stream it is launched on.
 
 Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--no-cpu-baseline]
        python bench.py --copy-calibration     (1 GiB copy for counter scaling)
+       python bench.py --audit-calls N        (N audit calls only, for counter passes)
        python bench.py --record-traffic DIR   (counter runs -> profiles/counters.json)
 """
 from __future__ import annotations
@@ -732,6 +733,34 @@ def copy_calibration(gib=1.0, reps=5):
                       "read_GBps": round(4 * n * 2 / (read_ms * 1e-3) / 1e9, 1)}), flush=True)
 
 
+def audit_calls(n):
+    """`n` plain pair_audit calls on the audit workload (B=256, G=16,
+    D=65536, R=4096), each followed by a synchronisation, and nothing else:
+    the program a matrix-core counter pass profiles."""
+    import torch
+
+    import paper_2608_11368_amd as pair
+    import workloads as wl
+
+    dev = torch.device("cuda:0")
+    wa = wl.WORKLOADS["audit"]
+    m = wl.host_meta(wa)
+    off, rew, p = (torch.from_numpy(a).to(dev) for a in (m.offsets, m.rewards, m.p))
+    s = wl.device_scores(wa, m.nv, dev)
+    ws = torch.empty(pair.pair_audit_workspace_bytes(m.B, m.gmax, wa.D, wa.R), dtype=torch.uint8,
+                     device=dev)
+    mse = torch.empty(m.B, dtype=torch.float64, device=dev)
+    bias = torch.empty_like(mse)
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+    for k in range(n):
+        pair.pair_audit(m.B, m.nv, m.gmax, off, s, rew, p, None, wa.design_seed, 0, wa.R, mse, bias,
+                        None, None, ws, st)
+        torch.cuda.synchronize()
+        if int(st.item()) != 0:
+            raise RuntimeError(f"device status {int(st.item())} in audit call {k}")
+        print(json.dumps({"audit_call": k, "mean_mse": float(mse.mean())}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -739,6 +768,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--audit-calls", type=int, default=0, metavar="N")
     ap.add_argument("--record-traffic", metavar="DIR",
                     help="write profiles/counters.json from rocprofv3 --pmc runs under DIR")
     args = ap.parse_args()
@@ -760,6 +790,9 @@ def main():
 
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.audit_calls > 0:
+        audit_calls(args.audit_calls)
         return
 
     dev = torch.device("cuda:0")
