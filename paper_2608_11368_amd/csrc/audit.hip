@@ -346,7 +346,8 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
   __shared__ int fbar;
   __shared__ uint32_t row_max[KP];
   __shared__ int32_t ex[KP];
-  static_assert(kSteps % 2 == 0 && SW % kMfmaThreads == 0 && KP <= kWave, "slice shape");
+  static_assert(kSteps % 2 == 0 && kSteps >= 4 && SW % kMfmaThreads == 0 && KP <= kWave,
+                "slice shape");
 
   // XCD-aware placement: hardware round-robins workgroup ids over 8 XCDs;
   // give each XCD a contiguous range of logical (prompt, slice) ids so the
@@ -507,12 +508,21 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
     f32x16_t accA[kPair], accB[kPair];
     float sq[kPair][4];
 #pragma unroll
-    for (int q = 0; q < kPair; ++q) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) accB[q][v] = 0.0f;
+    for (int q = 0; q < kPair; ++q)
 #pragma unroll
       for (int k = 0; k < 4; ++k) sq[q][k] = 0.0f;
-    }
+    auto first = [&](const f16x8_t (&Af)[KS], f32x16_t (&acc)[kPair]) {
+#pragma unroll
+      for (int q = 0; q < kPair; ++q) {
+        f32x16_t a;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) a[v] = 0.0f;
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+          a = __builtin_amdgcn_mfma_f32_32x32x16_f16(Af[s], Bt[q][s], a, 0, 0, 0);
+        acc[q] = a;
+      }
+    };
     auto step = [&](const f16x8_t (&Af)[KS], f32x16_t (&acc)[kPair], const f32x16_t (&prev)[kPair]) {
 #pragma unroll
       for (int q = 0; q < kPair; ++q) {
@@ -531,9 +541,15 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
       }
       __builtin_amdgcn_sched_barrier(0);
     };
+    // Step 0 has no previous step to square; steps 1 .. kSteps-1 each square
+    // the one before, and the last is squared after the loop.
     f16x8_t A0[KS], A1[KS];
     read_a(0, A0);
-    for (int st = 0; st < kSteps; st += 2) {
+    read_a(1, A1);
+    first(A0, accA);
+    read_a(2, A0);
+    step(A1, accB, accA);
+    for (int st = 2; st < kSteps; st += 2) {
       read_a(st + 1, A1);
       step(A0, accA, accB);
       if (st + 2 < kSteps) read_a(st + 2, A0);
