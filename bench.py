@@ -451,7 +451,7 @@ def time_wgrad_configs(pair, stream, wl, dev, coeff, out, scores, off, rew, p, m
 
 
 def time_alloc(pair, stream, wl, dev, reps=5):
-    """Probability design (Sec. 3.4) on the ragged workload's prompt structure
+    """Probability design (Sec. 4.4) on the ragged workload's prompt structure
     (B = 512, G_b ~ U{2..64}) with synthetic prefix statistics; each design
     timed with events on the launch stream."""
     import torch
@@ -568,7 +568,7 @@ def time_exact_audit(pair, stream, B, nv, G, off, scores, rew, p, D, reps=10):
 
 def audit_matrix(pair, stream, wl, dev, R=1000, D=4096):
     """The frozen-policy audit matrix (App. E; the procedure behind the audit
-    tables of Sec. 5.2) on a synthetic population: the ragged workload's
+    tables of Sec. 6.2) on a synthetic population: the ragged workload's
     prompt structure (B = 512, G_b ~ U{2..64}), rewards, prefix statistics and
     suffix lengths, with bf16 N(0, 1/D) scores of width D.  Each row's design
     is replayed over R draws against the complete-pair target: bias norm and

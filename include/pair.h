@@ -65,7 +65,7 @@ extern "C" {
                                 c or m not positive and finite)               */
 
 /* Edge-weight rules: the estimator variants compared in the paper's audit and
- * ablation tables (Sec. 5, Tables 2, 4, 5; App. A "Naive selection bias" and
+ * ablation tables (Sec. 6, Tables 2, 4, 5; App. A "Naive selection bias" and
  * App. B "Estimated and stabilized propensities").  Each rule estimates
  *     g = (1/N) sum_{i<j observed} 1/2 (r_i - r_j) (w_i s_i - w_j s_j):
  *   HT          w = 1/rho_ij,              N = M = C(G, 2)  exact PAIR, Eq. (pair-ht)
@@ -88,7 +88,7 @@ extern "C" {
 #define PAIR_RULE_MARGINAL 5
 
 /* Probability designs for pair_design_alloc. */
-#define PAIR_DESIGN_PAIR 0       /* graph-coupled convex design, Sec. 3.4        */
+#define PAIR_DESIGN_PAIR 0       /* graph-coupled convex design, Sec. 4.4        */
 #define PAIR_DESIGN_POINTWISE 1  /* pointwise p (1 - p) allocation               */
 #define PAIR_DESIGN_UNIFORM 2    /* one probability, the same expected cost      */
 
@@ -97,9 +97,9 @@ extern "C" {
 #define PAIR_GMAX_LIMIT 64
 
 /*
- * pair_design_inclusion -- randomized continuation design (paper Sec. 2.3,
- * Algorithm 1 "draw J_i with fresh randomization"; Theorem 2's requirement
- * that rho_ij is logged before rewards are seen).
+ * pair_design_inclusion -- randomized continuation design (paper Sec. 3.3;
+ * the design draw of Algorithm 1, a new independent draw per step; Theorem
+ * 2's requirement that rho_ij is logged before rewards are seen).
  *
  * Independent Bernoulli vertices: J_i ~ Bernoulli(p_i), I_ij = J_i J_j,
  * rho_ij = p_i p_j.  The indicators come from the counter-based generator
@@ -127,8 +127,8 @@ int pair_design_inclusion(int64_t B, int64_t nv, int32_t gmax, const int64_t* of
                           int32_t* d_status, void* stream);
 
 /*
- * pair_design_alloc -- graph-coupled probability design (paper Sec. 3.3 and
- * Sec. 3.4, Eqs. (disagreement), (edge-proxy), (convex-objective), (budget)):
+ * pair_design_alloc -- graph-coupled probability design (paper Sec. 4.3 and
+ * Sec. 4.4, Eqs. (disagreement), (edge-proxy), (convex-objective), (budget)):
  * continuation probabilities for every prompt from its prefix statistics.
  *     d_ij = p_i (1 - p_j) + (1 - p_i) p_j,  a_ij = d_ij [ (m_i + m_j)^2 / 4 ]
  *     b_i  = (sum_{j != i} sqrt(a_ij))^2 - sum_{j != i} a_ij
@@ -216,9 +216,9 @@ int pair_cps_draw(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, c
 
 /*
  * pair_edge_coeffs -- pair-corrected sequence advantages, paper Eq.
- * (pair-advantage) with the enumeration of Algorithm 1 ("accumulate
- * h_ij / rho_ij into A~_i, A~_j") and App. C's numerics (fp32 accumulation,
- * centred across the observed endpoints):
+ * (pair-advantage), each observed edge's weighted term added to both of its
+ * endpoints as in Algorithm 1's pair-corrected update, with App. C's numerics
+ * (fp32 accumulation, centred across the observed endpoints):
  *     A~_i = J_i / (2M) * sum_{j != i} J_j (r_i - r_j) / rho_ij,
  * then A~_i -= mean of A~ over completed vertices.  Unobserved vertices get
  * exactly 0, and so does every vertex of a prompt with fewer than two
@@ -239,7 +239,7 @@ int pair_edge_coeffs(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets
 
 /*
  * pair_design_coeffs -- the design draw of one replicate and the HT
- * coefficient fold in a single launch (paper Sec. 2.3 and Eq.
+ * coefficient fold in a single launch (paper Sec. 3.3 and Eq.
  * (pair-advantage), as pair_design_inclusion followed by pair_edge_coeffs on
  * its logged block).  The indicators, the logged rho_ij = fl32(p_i p_j) and
  * the coefficients are bitwise those of the two calls with R = 1 and
@@ -283,7 +283,7 @@ int pair_edge_coeffs_rule(int64_t B, int64_t nv, int32_t gmax, const int64_t* of
 
 /*
  * pair_weighted_grad -- the induced-edge HT gradient, paper Eq. (pair-ht)
- * written as sum_i A~_i s_i (Sec. 3.5), batched over prompts:
+ * written as sum_i A~_i s_i (Sec. 4.5), batched over prompts:
  *     reduce = 0:  out[b][d] = sum_{i < G_b} coeff[offsets[b] + i] * s[offsets[b] + i][d]
  *     reduce = 1:  out[d]    = (1/B) sum_b (the same per-prompt sum),
  * i.e. the batch mean of the per-prompt estimates, summed flat over the packed
@@ -312,7 +312,7 @@ int pair_weighted_grad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D,
 size_t pair_audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R);
 
 /*
- * pair_audit -- frozen-population estimator audit (paper Sec. 5.2, Table 2,
+ * pair_audit -- frozen-population estimator audit (paper Sec. 6.2, Table 2,
  * App. D metrics).  For each prompt the complete candidate population is
  * fixed; R design replicates rep0 .. rep0+R-1 are drawn exactly as
  * pair_design_inclusion draws them (same seed => same masks), each one gives
@@ -375,7 +375,7 @@ size_t pair_audit_direction_workspace_bytes(int64_t B, int32_t gmax, int64_t D, 
 
 /*
  * pair_audit_direction -- the update-direction column of the frozen-policy
- * audit (paper Sec. 5.2 lists the cosine among the audit metrics; the audit
+ * audit (paper Sec. 6.2 lists the cosine among the audit metrics; the audit
  * matrix of App. E reports it per design): for the replicates rep0 ..
  * rep0+R-1, drawn and folded exactly as pair_audit_rule draws and folds them,
  *     cos_r     = <g_r, t> / (|g_r| |t|)    (0 when g_r = 0 or t = 0)

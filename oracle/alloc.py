@@ -2,7 +2,7 @@
 the allocation solver; only tests/, the smoke check and the bench's CPU
 baseline may use it).
 
-Follows the paper's Sec. 3.3 (contrast graph) and Sec. 3.4 (graph-coupled
+Follows the paper's Sec. 4.3 (contrast graph) and Sec. 4.4 (graph-coupled
 probability design) in fp64:
 
   disagreement      d_ij = p_i (1 - p_j) + (1 - p_i) p_j          Eq. (disagreement)

@@ -11,19 +11,19 @@
  * Inputs are the exact fp32 / bf16 values the GPU sees, widened exactly.
  *
  * Paper sections followed:
- *   - Sec. 2.1, Eq. (loo)            leave-one-out gradient (used only by pins)
- *   - Sec. 2.2, Eq. (pair-kernel)    h_ij = 1/2 (r_i - r_j)(s_i - s_j)
- *   - Sec. 2.2, Eq. (pair-average)   complete-pair average, M = C(G,2)
- *   - Sec. 2.3                       adaptive continuation: J_i, I_ij = J_i J_j,
+ *   - Sec. 3.1, Eq. (loo)            leave-one-out gradient (used only by pins)
+ *   - Sec. 3.2, Eq. (pair-kernel)    h_ij = 1/2 (r_i - r_j)(s_i - s_j)
+ *   - Sec. 3.2, Eq. (pair-average)   complete-pair average, M = C(G,2)
+ *   - Sec. 3.3                       adaptive continuation: J_i, I_ij = J_i J_j,
  *                                    rho_ij = P(J_i J_j = 1), independent
  *                                    Bernoulli => rho_ij = pi_i pi_j, logged
- *   - Sec. 3.5, Eq. (pair-ht)        induced-edge Horvitz-Thompson estimator
- *   - Sec. 3.5, Eq. (pair-advantage) sequence advantages A~_i
- *   - Algorithm 1 (pair-corrected update): enumerate observed edges and
- *                                    accumulate h_ij / rho_ij into A~_i, A~_j
+ *   - Sec. 4.5, Eq. (pair-ht)        induced-edge Horvitz-Thompson estimator
+ *   - Sec. 4.5, Eq. (pair-advantage) sequence advantages A~_i
+ *   - Algorithm 1 (pair-corrected update): every observed edge adds its
+ *                                    1/rho-weighted term to both endpoints
  *   - App. B "At least two completed vertices": a draw with fewer than two
  *                                    completed vertices contributes zero
- *   - Sec. 5.2 frozen-policy audit and App. D metrics: MSE = E||g^ - g_full||^2,
+ *   - Sec. 6.2 frozen-policy audit and App. D metrics: MSE = E||g^ - g_full||^2,
  *                                    bias = || mean_r g^_r - g_full ||,
  *                                    ESS = (sum_e w_e)^2 / sum_e w_e^2
  *   - App. A "Naive selection bias" and App. B "Estimated and stabilized
@@ -151,7 +151,7 @@ static int check_offsets(int64_t B, const int64_t* offsets, int32_t gmax) {
 }
 
 /* ------------------------------------------------------------------------ */
-/* Design draw (Sec. 2.3): independent Bernoulli continuation with logged    */
+/* Design draw (Sec. 3.3): independent Bernoulli continuation with logged    */
 /* joint inclusion probabilities rho_ij = pi_i pi_j.                         */
 /*   mask[r][v]        J for vertex v in replicate rep0 + r                  */
 /*   pi[b][i][j]       fp32 rho_ij (i != j), pi_i on the diagonal, 0 beyond  */
@@ -402,7 +402,7 @@ int orc_pair_coeffs(int64_t B, const int64_t* offsets, int32_t gmax, const float
 }
 
 /* ------------------------------------------------------------------------ */
-/* Frozen-population audit (Sec. 5.2, App. D).  For each prompt:             */
+/* Frozen-population audit (Sec. 6.2, App. D).  For each prompt:             */
 /*   target  t   = complete-pair average, Eq. (pair-average)                 */
 /*   for r in [rep0, rep0 + R): draw J^(r) as orc_design_inclusion does,     */
 /*       g_r = the estimate under `rule` (Eq. (pair-ht) for the HT rule),    */
@@ -411,7 +411,7 @@ int orc_pair_coeffs(int64_t B, const int64_t* offsets, int32_t gmax, const float
 /*       e_r = || g_r - t ||^2                                               */
 /*   mse  = (1/R) sum_r e_r ;  bias = || (1/R) sum_r g_r - t ||              */
 /* rep_sqerr[b][R] and edge_count[b][R] are optional per-replicate outputs. */
-/* Update direction (Sec. 5.2 and the audit matrix of App. E: the cosine    */
+/* Update direction (Sec. 6.2 and the audit matrix of App. E: the cosine    */
 /* between an estimate and the target): cos_r = <g_r, t> / (|g_r| |t|),     */
 /* taken as 0 when either vector is zero (a draw with no observed edge, or  */
 /* a prompt whose target vanishes); cosine[b] = (1/R) sum_r cos_r and       */

@@ -1,4 +1,4 @@
-// Graph-coupled probability design (paper Sec. 3.3-3.4): continuation
+// Graph-coupled probability design (paper Sec. 4.3-4.4): continuation
 // probabilities from the prefix statistics, batched over prompts.
 //
 //   d_ij = p_i (1 - p_j) + (1 - p_i) p_j                 Eq. (disagreement)

@@ -1,4 +1,4 @@
-// Frozen-population estimator audit (paper Sec. 5.2, Table 2; App. D
+// Frozen-population estimator audit (paper Sec. 6.2, Table 2; App. D
 // metrics MSE = E||g^ - g_full||^2 and the bias norm).
 //
 // The complete-pair target of a prompt is itself a combination of its score
@@ -680,7 +680,7 @@ __global__ __launch_bounds__(256) void audit_final_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Update direction (Sec. 5.2 audit metrics; the Cosine column of the audit
+// Update direction (Sec. 6.2 audit metrics; the Cosine column of the audit
 // matrix, App. E).  Replicate r's estimate is g_r = u_r S_b with
 // u_r = delta_r + a (its fold's coefficients) and the target is t = a S_b, so
 // with the fp64 Gram matrix K = S_b S_b^T

@@ -1,6 +1,6 @@
 // Design draw: independent Bernoulli continuation indicators and the logged
-// joint inclusion probabilities (paper Sec. 2.3; Algorithm 1, "draw J_i with
-// fresh randomization"; rho_ij must be logged before rewards, Theorem 2).
+// joint inclusion probabilities (paper Sec. 3.3; the design draw of Algorithm
+// 1, new for every step; rho_ij must be logged before rewards, Theorem 2).
 //
 // One 64-lane wavefront per (replicate, prompt) unit, lane i = vertex i.  Each
 // lane evaluates Philox4x64-10 at counter (r, b, i >> 2, 0) and keeps word

@@ -1,5 +1,5 @@
 // Weighted-gradient stream: the induced-edge HT gradient of paper Eq.
-// (pair-ht) in its sequence-advantage form (Sec. 3.5),
+// (pair-ht) in its sequence-advantage form (Sec. 4.5),
 //     out[b][:] = sum_i A~_{b,i} s_{b,i,:},
 // batched over prompts, fp32 accumulation over fp32 or bf16 score rows.
 //

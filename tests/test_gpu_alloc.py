@@ -1,4 +1,4 @@
-"""GPU parity for the probability design (Sec. 3.3-3.4) through the C ABI,
+"""GPU parity for the probability design (Sec. 4.3-4.4) through the C ABI,
 against the allocation oracle (SLSQP in fp64 on the same program).
 
 Bars: the design is an optimisation, so the GPU result is checked as an

@@ -160,7 +160,7 @@ def test_full_size_exact_audit_and_monte_carlo_consistency():
 
 
 def test_audit_at_the_papers_fifty_thousand_draws():
-    """The Monte-Carlo audit at the paper's draw count (R = 50,000; Sec. 5.2)
+    """The Monte-Carlo audit at the paper's draw count (R = 50,000; Sec. 6.2)
     on 64 prompts of the audit workload at full width: every prompt's MSE
     within 5 standard errors of its exact Prop. 1 value, the bias norm of the
     unbiased HT estimator at the sqrt(MSE / R) scale, and the replicate range

@@ -1,4 +1,4 @@
-"""Pins for the allocation oracle (Sec. 3.3-3.4): the contrast-graph proxy,
+"""Pins for the allocation oracle (Sec. 4.3-4.4): the contrast-graph proxy,
 the vertex term's bound (App. A "Variance upper bound and convexity"), and
 the design solver's optimum checked independently of the solver -- KKT
 conditions, closed forms, feasible alternatives -- plus the paper's trace

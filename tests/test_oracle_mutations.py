@@ -16,10 +16,10 @@ normaliser, the rho entry and the edge mask of the estimator (Eq. pair-ht);
 the half-edge split of the sequence advantages (Eq. pair-advantage); the
 Philox reading of the design draw (word, counter layout, key schedule), the
 induced-edge count and the logged rho block; bf16 widening; the audit's
-target, MSE, bias and update-direction cosine (App. D, Sec. 5.2); the exact covariance trace of Prop. 1; the
+target, MSE, bias and update-direction cosine (App. D, Sec. 6.2); the exact covariance trace of Prop. 1; the
 conditional-Poisson inclusion probabilities; and the contrast graph's
 disagreement, edge proxy and vertex term, the design objective, its gradient
-and budget, and the pointwise and uniform comparison designs (Sec. 3.3-3.4).
+and budget, and the pointwise and uniform comparison designs (Sec. 4.3-4.4).
 """
 import concurrent.futures
 import os

@@ -113,7 +113,7 @@ def test_design_draw_logged_rho_and_edge_counts():
 
 
 def test_design_draw_inclusion_frequency_matches_p():
-    """Sec. 2.3: P(J_i = 1) = pi_i.  Binomial z-test over many replicates."""
+    """Sec. 3.3: P(J_i = 1) = pi_i.  Binomial z-test over many replicates."""
     offsets = np.array([0, 16], dtype=np.int64)
     p = np.linspace(0.05, 1.0, 16).astype(np.float32)
     R = 40000
