@@ -876,7 +876,12 @@ def main():
     bytes_dense = nv * D * 2 + nv * 4 + (B + 1) * 8 + B * D * 4
     gbps_chain = bytes_wgrad / (ms_chain * 1e-3) / 1e9
     gbps_wgrad = bytes_wgrad / (ms_wgrad * 1e-3) / 1e9
-    flops_audit = 2.0 * Ba * R * Ga * Da
+    # The audit sweeps only prompts whose rewards are not all equal: a prompt
+    # with equal rewards has zero deviations in every replicate, and its
+    # e_r, MSE and bias are exact zeros without any matrix work.
+    live_a = int(sum(np.ptp(meta_a.rewards[meta_a.offsets[b]:meta_a.offsets[b + 1]]) > 0
+                     for b in range(Ba)))
+    flops_audit = 2.0 * live_a * R * Ga * Da
     tflops_audit = flops_audit / (ms_audit * 1e-3) / 1e12
 
     roof_w = {"kernel": "wgrad_kernel<bf16> (pair_weighted_grad)", "bound": "hbm",
@@ -888,7 +893,11 @@ def main():
               "achieved": round(tflops_audit, 1), "peak": BF16_MFMA_PEAK_TFLOPS,
               "unit": "TFLOP/s", "frac": round(tflops_audit / BF16_MFMA_PEAK_TFLOPS, 4),
               "traffic": _traffic("audit_b256", ["audit.hip", "common.hpp"]),
-              "ms": round(ms_audit, 4), "flops": flops_audit}
+              "ms": round(ms_audit, 4), "flops": flops_audit,
+              "flops_note": "2*G*D per replicate estimate of the swept prompts",
+              "swept_prompts": live_a, "swept_fraction": round(live_a / Ba, 4),
+              "frac_if_all_prompts_counted": round(
+                  2.0 * Ba * R * Ga * Da / (ms_audit * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4)}
 
     result = {
         "metric": METRIC,

@@ -11,11 +11,16 @@ import of the library fails loudly (build it with
 
 The lower-case helpers (``design_inclusion``, ``edge_coeffs``,
 ``weighted_grad``, ``audit``) allocate the outputs with torch and call the
-``pair_*`` functions.
+``pair_*`` functions.  Given an explicit ``stream``, a helper makes it torch's
+current stream while it allocates, clears and launches, so the zero-fills are
+ordered before the kernels and the caching allocator hands a temporary
+workspace to later work only behind them.
 """
 from __future__ import annotations
 
 import ctypes
+import functools
+import inspect
 import os
 
 import torch
@@ -323,6 +328,24 @@ def _nv(offsets):
     return int(offsets[-1].item())
 
 
+def _allocating(fn):
+    """Run an allocating helper with its `stream` argument (when given) as
+    torch's current stream: outputs, status words and temporary workspaces
+    are then allocated and zero-filled on the stream the kernels run on."""
+    sig = inspect.signature(fn)
+
+    @functools.wraps(fn)
+    def wrapper(*args, **kwargs):
+        stream = sig.bind(*args, **kwargs).arguments.get("stream")
+        if stream is None:
+            return fn(*args, **kwargs)
+        with torch.cuda.stream(stream):
+            return fn(*args, **kwargs)
+
+    return wrapper
+
+
+@_allocating
 def design_inclusion(offsets, p, seed, rep0, R, gmax, want_mask=True, want_pi=True, nv=None,
                      stream=None):
     B = offsets.numel() - 1
@@ -340,6 +363,7 @@ def design_inclusion(offsets, p, seed, rep0, R, gmax, want_mask=True, want_pi=Tr
     return out
 
 
+@_allocating
 def design_coeffs(offsets, p, rewards, seed, rep, gmax, want_mask=True, want_pi=True, nv=None,
                   stream=None):
     """One replicate's design draw and its sequence advantages A~ in one
@@ -361,6 +385,7 @@ def design_coeffs(offsets, p, rewards, seed, rep, gmax, want_mask=True, want_pi=
     return out
 
 
+@_allocating
 def edge_coeffs(offsets, rewards, mask, pi, gmax, nv=None, rule=None, wmax=0.0, stream=None):
     """Coefficients; with `rule` (RULE_*) also returns the ESS and the maximum weight."""
     B = offsets.numel() - 1
@@ -379,6 +404,7 @@ def edge_coeffs(offsets, rewards, mask, pi, gmax, nv=None, rule=None, wmax=0.0, 
     return {"coeff": coeff, "edge_count": ec, "ess": ess, "max_weight": mw, "status": st}
 
 
+@_allocating
 def weighted_grad(offsets, scores, coeff, nv=None, reduce=False, stream=None):
     B = offsets.numel() - 1
     nv = _nv(offsets) if nv is None else nv
@@ -390,6 +416,7 @@ def weighted_grad(offsets, scores, coeff, nv=None, reduce=False, stream=None):
     return {"out": out, "status": st}
 
 
+@_allocating
 def audit(offsets, scores, rewards, p, seed, rep0, R, gmax, pi_w=None, want_reps=True, nv=None,
           workspace=None, rule=None, wmax=0.0, stream=None):
     B = offsets.numel() - 1
@@ -416,6 +443,7 @@ def audit(offsets, scores, rewards, p, seed, rep0, R, gmax, pi_w=None, want_reps
     return out
 
 
+@_allocating
 def audit_direction(offsets, scores, rewards, p, seed, rep0, R, gmax, pi_w=None, rule=RULE_HT,
                     wmax=0.0, nv=None, workspace=None, stream=None):
     """Mean per-replicate cosine between estimate and target, and |t|."""
@@ -435,6 +463,7 @@ def audit_direction(offsets, scores, rewards, p, seed, rep0, R, gmax, pi_w=None,
     return out
 
 
+@_allocating
 def audit_exact(offsets, scores, rewards, p, gmax, pi_w=None, rule=RULE_HT, wmax=0.0,
                 want_gram=False, nv=None, workspace=None, stream=None):
     """Exact design MSE and bias norm per prompt (no draws); optional Gram."""
@@ -455,6 +484,7 @@ def audit_exact(offsets, scores, rewards, p, gmax, pi_w=None, rule=RULE_HT, wmax
     return out
 
 
+@_allocating
 def design_alloc(offsets, p_hat, c_hat, budget, gmax, pi_min=0.08, design=DESIGN_PAIR, m_hat=None,
                  nv=None, stream=None):
     """Continuation probabilities of every prompt (fp32 [nv]) with the
@@ -473,6 +503,7 @@ def design_alloc(offsets, p_hat, c_hat, budget, gmax, pi_min=0.08, design=DESIGN
     return out
 
 
+@_allocating
 def cps_fit(offsets, pi_target, gmax, nv=None, stream=None):
     """Fixed-size design from target probabilities: dict(w, n, pi_joint, iters, status)."""
     B = offsets.numel() - 1
@@ -490,6 +521,7 @@ def cps_fit(offsets, pi_target, gmax, nv=None, stream=None):
     return out
 
 
+@_allocating
 def cps_draw(offsets, w, n, seed, rep0, R, gmax, nv=None, stream=None):
     """Fixed-size draws: dict(mask[R][nv], edge_count[R][B], status)."""
     B = offsets.numel() - 1

@@ -18,7 +18,12 @@
 //                   fixed-order partial sum of delta over the 256 lanes.
 //  2. audit_prep    replicate rows padded with zero rows to a whole number
 //                   of tile pairs (R rounded up to 64), delta_bar stored
-//                   in the row after them.
+//                   in the row after them.  One extra workgroup lists the
+//                   live prompts in ascending order: those whose rewards are
+//                   not all equal.  A prompt with equal rewards has
+//                   W = 0 and a = 0, so every delta_r is exactly zero and so
+//                   are its e_r, MSE and bias; the matrix-core grid covers
+//                   the live prompts only.
 //  3. audit_mfma    the contraction on v_mfma_f32_32x32x16_f16.  Each score
 //                   row of a column slice is rescaled by 2^-e_i, with e_i
 //                   the exponent of the row's largest magnitude within the
@@ -33,12 +38,15 @@
 //                   replicate row sweeps over it, so S_b is read from HBM
 //                   once; the squares of every output tile are summed in the
 //                   epilogue and the rows x D product is never written.
-//                   Workgroups of one prompt are placed on one XCD so its
-//                   delta rows are shared through that XCD's L2.  The
+//                   The live (prompt, slice) pairs are split evenly over the
+//                   8 XCDs, each XCD taking a contiguous range, so the
+//                   workgroups of a prompt share that XCD's L2 for its delta
+//                   rows.  The
 //                   delta_bar row is one fp32 dot product per score column
 //                   on the vector units against the same LDS slice.
 //  4. audit_sqerr   e_r = per-slice partial sums reduced in fixed order, one
-//                   thread per (prompt, replicate); fp64 partial sums of e_r
+//                   thread per (prompt, replicate), exactly 0 for a prompt
+//                   that is not live; fp64 partial sums of e_r
 //     audit_final   per prompt: MSE = fp64 mean of e_r, bias = sqrt(e of the
 //                   delta_bar row).
 #include "common.hpp"
@@ -74,7 +82,7 @@ struct AuditLayout {
   int64_t nslices;   // score-column slices per prompt
   int64_t nwg;       // audit_coeffs workgroups per prompt
   int64_t nsq;       // audit_sqerr workgroups per prompt
-  size_t delta_off, epart_off, dsum_off, rpart_off, ebar_off, total;
+  size_t delta_off, epart_off, dsum_off, rpart_off, ebar_off, live_off, total;
 };
 
 AuditLayout audit_layout(int64_t B, int32_t gmax, int64_t D, int64_t R) {
@@ -98,6 +106,8 @@ AuditLayout audit_layout(int64_t B, int32_t gmax, int64_t D, int64_t R) {
   off += (size_t)round_up(B * L.nsq * 8, 256);                      // fp64 partial sums of e_r
   L.ebar_off = off;
   off += (size_t)round_up(B * 4, 256);                              // e of the delta_bar row
+  L.live_off = off;
+  off += (size_t)round_up((2 * B + 1) * 4, 256);                    // live count, list, flags
   L.total = off;
   return L;
 }
@@ -282,13 +292,58 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
 // ---------------------------------------------------------------------------
 // 2. delta_bar row and zero padding.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void audit_prep_kernel(int64_t B, int64_t nv, int32_t gmax, int kp,
-                                                         const int64_t* __restrict__ offsets,
-                                                         int64_t R, int64_t rbar, int64_t nwg,
-                                                         int64_t rrows,
-                                                         const float* __restrict__ dsum,
-                                                         float* __restrict__ delta) {
+constexpr int kPrepThreads = 256;
+
+// Live prompts: live[0] = their count, live[1 ..] = their indices in
+// ascending order, live[1 + B + b] = 1 if prompt b is live, else 0.  A prompt
+// is live when its group is valid and some reward differs from the first (a
+// NaN reward counts as different).  One workgroup, chunks of 256 prompts, a
+// ballot prefix count within each wave and the waves in order.
+__device__ void list_live_prompts(int64_t B, int64_t nv, int32_t gmax,
+                                  const int64_t* __restrict__ offsets,
+                                  const float* __restrict__ rewards, int32_t* __restrict__ live) {
+  constexpr int kWaves = kPrepThreads / kWave;
+  __shared__ int32_t wcount[kWaves];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  int32_t base = 0;
+  for (int64_t c0 = 0; c0 < B; c0 += kPrepThreads) {
+    const int64_t b = c0 + tid;
+    bool lv = false;
+    if (b < B) {
+      int64_t o0, g;
+      if (prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, nullptr, false)) {
+        const float r0 = rewards[o0];
+        for (int64_t i = 1; i < g; ++i) lv = lv || !(rewards[o0 + i] == r0);
+      }
+      live[1 + B + b] = lv ? 1 : 0;
+    }
+    const uint64_t m = __ballot(lv);
+    const int before = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == 0) wcount[wave] = __popcll(m);
+    __syncthreads();
+    int32_t off = base, tot = 0;
+    for (int w = 0; w < kWaves; ++w) {
+      if (w < wave) off += wcount[w];
+      tot += wcount[w];
+    }
+    if (lv) live[1 + off + before] = (int32_t)b;
+    base += tot;
+    __syncthreads();
+  }
+  if (tid == 0) live[0] = base;
+}
+
+__global__ __launch_bounds__(kPrepThreads) void audit_prep_kernel(
+    int64_t B, int64_t nv, int32_t gmax, int kp, const int64_t* __restrict__ offsets,
+    const float* __restrict__ rewards, int64_t R, int64_t rbar, int64_t nwg, int64_t rrows,
+    const float* __restrict__ dsum, float* __restrict__ delta, int32_t* __restrict__ live) {
   const int64_t b = blockIdx.x;
+  if (b == B) {
+    list_live_prompts(B, nv, gmax, offsets, rewards, live);
+    return;
+  }
   int64_t o0, g;
   if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, nullptr, false)) return;
   const int tid = threadIdx.x;
@@ -332,8 +387,8 @@ template <int KS>
 __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS == 1 ? 4 : 2))) void audit_mfma_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets, int64_t D,
     const uint16_t* __restrict__ scores, int64_t ld, int64_t rrows, int64_t ntiles,
-    int64_t nslices, const float* __restrict__ delta, float* __restrict__ epart,
-    int32_t* d_status) {
+    int64_t nslices, const float* __restrict__ delta, const int32_t* __restrict__ live,
+    float* __restrict__ epart, int32_t* d_status) {
   constexpr int KP = 16 * KS;
   constexpr int SW = slice_cols(KS);
   constexpr int kSteps = SW / kTile;
@@ -349,14 +404,19 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
   static_assert(kSteps % 2 == 0 && kSteps >= 4 && SW % kMfmaThreads == 0 && KP <= kWave,
                 "slice shape");
 
-  // XCD-aware placement: hardware round-robins workgroup ids over 8 XCDs;
-  // give each XCD a contiguous range of logical (prompt, slice) ids so the
-  // workgroups of a prompt share that XCD's L2 for the delta rows.
-  const int64_t per_xcd = gridDim.x / 8;
-  const int64_t L = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (L >= B * nslices) return;
-  const int64_t b = L / nslices;
-  const int64_t sl = L - b * nslices;
+  // XCD-aware placement: hardware round-robins workgroup ids over 8 XCDs.
+  // The grid has room for every prompt; the n live (prompt, slice) pairs are
+  // split into 8 contiguous ranges of ceil(n / 8), one per XCD, so the
+  // workgroups of a prompt share that XCD's L2 for the delta rows and the
+  // XCDs get equal work.  Workgroups beyond the live work exit at once.
+  const int64_t n_live = (int64_t)live[0] * nslices;
+  const int64_t per_xcd = (n_live + 7) / 8;
+  const int64_t j = blockIdx.x / 8;
+  if (j >= per_xcd) return;
+  const int64_t L = (int64_t)(blockIdx.x % 8) * per_xcd + j;
+  if (L >= n_live) return;
+  const int64_t b = live[1 + L / nslices];
+  const int64_t sl = L - (L / nslices) * nslices;
   int64_t o0, g;
   if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, nullptr, false)) return;
 
@@ -630,15 +690,17 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
 __global__ __launch_bounds__(kSqThreads) void audit_sqerr_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets, int64_t R,
     int64_t rbar, int64_t rrows, int64_t nslices, int64_t nsq, const float* __restrict__ epart,
-    double* __restrict__ rpart, float* __restrict__ ebar, float* __restrict__ rep_sqerr) {
+    const int32_t* __restrict__ live, double* __restrict__ rpart, float* __restrict__ ebar,
+    float* __restrict__ rep_sqerr) {
   __shared__ double part[kSqThreads / kWave];
   const int64_t b = blockIdx.x / nsq;
   const int64_t c = blockIdx.x - b * nsq;
   int64_t o0, g;
   if (!prompt_bounds(offsets, b, nv, 2, gmax, &o0, &g, nullptr, false)) return;
   const int64_t r = c * kSqThreads + threadIdx.x;
+  const bool is_live = live[1 + B + b] != 0;   // not live: every delta_r is 0, so e_r = 0
   float e = 0.0f;
-  if (r <= R) {
+  if (r <= R && is_live) {
     const float* eb = epart + b * nslices * rrows + (r < R ? r : rbar);
     int64_t k = 0;
     for (; k + 8 <= nslices; k += 8) {
@@ -649,9 +711,9 @@ __global__ __launch_bounds__(kSqThreads) void audit_sqerr_kernel(
       for (int q = 0; q < 8; ++q) e += v[q];
     }
     for (; k < nslices; ++k) e += eb[k * rrows];
-    if (r < R && rep_sqerr != nullptr) rep_sqerr[b * R + r] = e;
-    if (r == R) ebar[b] = e;
   }
+  if (r < R && rep_sqerr != nullptr) rep_sqerr[b * R + r] = e;
+  if (r == R) ebar[b] = e;
   double s = r < R ? (double)e : 0.0;
 #pragma unroll
   for (int m = 1; m < kWave; m <<= 1) s += __shfl_xor(s, m, kWave);
@@ -876,10 +938,16 @@ int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, in
   float* dsum = reinterpret_cast<float*>(ws + L.dsum_off);
   double* rpart = reinterpret_cast<double*>(ws + L.rpart_off);
   float* ebar = reinterpret_cast<float*>(ws + L.ebar_off);
+  int32_t* live = reinterpret_cast<int32_t*>(ws + L.live_off);
   const uint16_t* s = static_cast<const uint16_t*>(scores);
 
+  // Every grid size is checked before the first launch.
   const int64_t coef_grid = B * L.nwg;
-  if (coef_grid > 0x7fffffffLL) return PAIR_ERANGE;
+  const int64_t grid = round_up(B * L.nslices, 8);
+  const int64_t sq_grid = B * L.nsq;
+  if (coef_grid > 0x7fffffffLL || B + 1 > 0x7fffffffLL || grid > 0x7fffffffLL ||
+      sq_grid > 0x7fffffffLL)
+    return PAIR_ERANGE;
 #define PAIR_AUDIT_COEFFS(KP_)                                                                  \
   hipLaunchKernelGGL(audit_coeffs_kernel<KP_>, dim3((unsigned)coef_grid), dim3(kCoefThreads), 0, \
                      stream, B, nv, gmax, offsets, rewards, p, pi_w, rule, wmax, seed, rep0, R,  \
@@ -893,16 +961,15 @@ int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, in
 #undef PAIR_AUDIT_COEFFS
   if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
 
-  hipLaunchKernelGGL(audit_prep_kernel, dim3((unsigned)B), dim3(256), 0, stream, B, nv, gmax, L.kp,
-                     offsets, R, L.rbar, L.nwg, L.rrows, dsum, delta);
+  hipLaunchKernelGGL(audit_prep_kernel, dim3((unsigned)(B + 1)), dim3(kPrepThreads), 0, stream, B,
+                     nv, gmax, L.kp, offsets, rewards, R, L.rbar, L.nwg, L.rrows, dsum, delta,
+                     live);
   if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
 
-  const int64_t grid = round_up(B * L.nslices, 8);
-  if (grid > 0x7fffffffLL) return PAIR_ERANGE;
 #define PAIR_AUDIT_MFMA(KS_)                                                                   \
   hipLaunchKernelGGL(audit_mfma_kernel<KS_>, dim3((unsigned)grid), dim3(kMfmaThreads), 0, stream, \
-                     B, nv, gmax, offsets, D, s, ld, L.rrows, L.ntiles, L.nslices, delta, epart, \
-                     d_status)
+                     B, nv, gmax, offsets, D, s, ld, L.rrows, L.ntiles, L.nslices, delta, live,   \
+                     epart, d_status)
   switch (L.ks) {
     case 1: PAIR_AUDIT_MFMA(1); break;
     case 2: PAIR_AUDIT_MFMA(2); break;
@@ -912,11 +979,9 @@ int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, in
 #undef PAIR_AUDIT_MFMA
   if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
 
-  const int64_t sq_grid = B * L.nsq;
-  if (sq_grid > 0x7fffffffLL) return PAIR_ERANGE;
   hipLaunchKernelGGL(audit_sqerr_kernel, dim3((unsigned)sq_grid), dim3(kSqThreads), 0, stream, B,
-                     nv, gmax, offsets, R, L.rbar, L.rrows, L.nslices, L.nsq, epart, rpart, ebar,
-                     rep_sqerr);
+                     nv, gmax, offsets, R, L.rbar, L.rrows, L.nslices, L.nsq, epart, live, rpart,
+                     ebar, rep_sqerr);
   if (hipGetLastError() != hipSuccess) return PAIR_EHIP;
   hipLaunchKernelGGL(audit_final_kernel, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, stream,
                      B, nv, gmax, offsets, R, L.nsq, rpart, ebar, mse, bias_norm);

@@ -153,7 +153,6 @@ __global__ __launch_bounds__(kWave) void cps_fit_kernel(
   bool have_base = false;
   int it = 0;
   bool converged = false;
-  double* A = Pf;   // the Newton system reuses the prefix table's storage
   for (; it < kMaxFitIter; ++it) {
     w = unit ? exp(th) : 0.0;
     // pi_i(w) for every unit from the prefix and suffix polynomial tables.
@@ -169,7 +168,7 @@ __global__ __launch_bounds__(kWave) void cps_fit_kernel(
     }
     const double f = wave_sum_d(unit ? t * th : 0.0) - log(en);
     const double err = wave_max_d(unit ? fabs(pi / t - 1.0) : 0.0);
-    __syncthreads();   // every lane has read the tables before A overwrites them
+    __syncthreads();   // every lane has read the tables before the Newton system overwrites them
     if (have_base) {
       const bool ok = isfinite(f) && isfinite(err) &&
                       (f >= f0 + 1e-4 * step * slope || err < err0);

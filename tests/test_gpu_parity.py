@@ -26,13 +26,16 @@ import torch
 import oracle
 import paper_2608_11368_amd as pair
 import workloads as wl
-from tests.gpu_util import DEV, log, rel_l2, scores_to_device, scores_to_host, upload_meta
+from tests.gpu_util import (DEV, log, rel_l2, scores_to_device, scores_to_host, tile_columns,
+                            upload_meta)
 
 pytestmark = pytest.mark.gpu
 
 FP32_TOL = 1e-5
 BF16_TOL = 2e-3
 BIAS_TOL = 5e-5
+# Columns per workgroup tile of the bf16 weighted-gradient kernel.
+WGRAD_TILE_BF16 = 4096
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -217,14 +220,16 @@ def test_weighted_grad_edge_cases():
 def test_fewer_than_two_completed_gives_exact_zero():
     w = wl.WORKLOADS["b128"].replace(B=16, D=512)
     meta = wl.host_meta(w)
-    meta.p[:] = np.float32(0.02)          # almost every draw completes < 2 vertices
+    meta.p[:] = np.float32(0.02)          # almost every draw completes < 2 vertices ...
+    meta.p[12 * 16:] = np.float32(0.9)    # ... except in the last four prompts,
+    meta.rewards[12 * 16:] = np.arange(4 * 16) % 2   # which have unequal rewards
     log("k<2 zero prompts")
     dm = upload_meta(meta)
     s = wl.host_scores(w, meta.nv)
     d, c, g = _chain_gpu(meta, dm, scores_to_device(s, w), 77, meta.gmax)
     od, est, _ = _chain_oracle(meta, s, 77, meta.gmax)
     k = d["completed"].cpu().numpy()[0]
-    assert np.any(k < 2)
+    assert np.any(k < 2) and np.any(k >= 2)
     out = g["out"].cpu().numpy()
     for b in range(meta.B):
         if k[b] < 2:
@@ -232,19 +237,21 @@ def test_fewer_than_two_completed_gives_exact_zero():
     assert rel_l2(out, est) <= BF16_TOL
 
 
-@pytest.mark.parametrize("name,ncols", [("b128", 2048), ("ragged", 1024), ("qwen3", 256)])
-def test_full_size_sampled_columns(name, ncols):
+@pytest.mark.parametrize("name", ["b128", "ragged", "qwen3"])
+def test_full_size_sampled_columns(name):
     """The workload at its full size, in the launch configuration the bench
-    times; the oracle recomputes a random sample of columns (plus the last
-    ones) from the same device-resident scores."""
+    times; the oracle recomputes sampled columns from the same
+    device-resident scores: a random column inside every 4096-column tile
+    the bf16 kernel writes (16,384 tiles for the 2^26-column workload), the
+    first and last column of every 16th tile, and the last 16 columns."""
     w = wl.WORKLOADS[name]
     meta = wl.host_meta(w)
     log(f"full size {name} B={meta.B} nv={meta.nv} D={w.D}")
     dm = upload_meta(meta)
     sd = wl.device_scores(w, meta.nv, DEV)
     d, c, g = _chain_gpu(meta, dm, sd, w.design_seed, meta.gmax)
-    rng = np.random.default_rng(3)
-    cols = np.unique(np.concatenate([rng.choice(w.D, ncols, replace=False), np.arange(w.D - 16, w.D)]))
+    cols = tile_columns(w.D, WGRAD_TILE_BF16, np.random.default_rng(3))
+    log(f"  {cols.size} sampled columns")
     ci = torch.from_numpy(cols).to(DEV)
     s_host = scores_to_host(sd.index_select(1, ci))
     out = g["out"].index_select(1, ci).cpu().numpy()
@@ -253,6 +260,12 @@ def test_full_size_sampled_columns(name, ncols):
     err = rel_l2(out, est)
     log(f"  sampled grad rel L2 = {err:.3e}")
     assert err <= BF16_TOL
+    # every prompt with a nonzero estimate is compared on its own too
+    live = np.linalg.norm(est, axis=1) > 0
+    assert live.sum() >= meta.B // 2
+    per = [rel_l2(out[b], est[b]) for b in np.flatnonzero(live)]
+    log(f"  worst prompt rel L2 = {max(per):.3e} over {live.sum()} prompts")
+    assert max(per) <= BF16_TOL
     _assert_zero_rows(meta, c["coeff"], g["out"])
     assert torch.isfinite(g["out"]).all()
     del sd, g
@@ -553,6 +566,50 @@ def test_audit_uneven_split_is_bitwise_one_call():
     assert torch.equal(torch.cat([part["edge_count"] for part in parts], dim=1), one["edge_count"])
 
 
+def test_audit_equal_reward_prompts():
+    """Prompts whose rewards are all equal have zero deviations in every
+    replicate: exact zeros for e_r, MSE and bias, their edge counts still
+    drawn, and their score rows never read (NaN there raises nothing).  The
+    other prompts match the oracle.  A non-finite score in a prompt that is
+    swept sets PAIR_ST_NONFINITE."""
+    w = wl.WORKLOADS["audit"].replace(B=9, D=3000, dtype=wl.BF16)
+    meta = wl.host_meta(w)
+    G = 16
+    for b, v in ((1, 1.0), (4, 0.0), (8, 0.37)):
+        meta.rewards[b * G:(b + 1) * G] = v
+    live = np.ptp(meta.rewards.reshape(meta.B, G), axis=1) > 0
+    assert live.sum() >= 3
+    s = wl.host_scores(w, meta.nv)
+    s_nan = s.copy()
+    s_nan[4 * G:5 * G, ::7] = 0x7FC0                     # NaN in a prompt that is not swept
+    dm = upload_meta(meta)
+    R = 130
+    log(f"audit with equal-reward prompts B={meta.B} live={int(live.sum())}")
+    got = pair.audit(dm["offsets"], scores_to_device(s_nan, w), dm["rewards"], dm["p"],
+                     w.design_seed, 3, R, meta.gmax, nv=meta.nv)
+    torch.cuda.synchronize()
+    want = oracle.audit(meta.offsets, s, meta.rewards, meta.p, w.design_seed, 3, R)
+    assert int(got["status"].item()) == 0
+    assert np.array_equal(got["edge_count"].cpu().numpy(), want["edge_count"])
+    reps = got["rep_sqerr"].cpu().numpy()
+    for name in ("mse", "bias_norm"):
+        assert np.all(got[name].cpu().numpy()[~live] == 0.0) and np.all(want[name][~live] == 0.0)
+    assert np.all(reps[~live] == 0.0)
+    sub = {k: got[k][torch.from_numpy(live).to(DEV)] for k in ("mse", "bias_norm", "rep_sqerr",
+                                                                 "edge_count")}
+    sub["status"] = got["status"]
+    want_live = {k: want[k][live] for k in ("mse", "bias_norm", "rep_sqerr", "edge_count")}
+    _check_audit(sub, want_live, "live prompts")
+    # a NaN score in a swept prompt is reported
+    b_live = int(np.flatnonzero(live)[0])
+    s_bad = s.copy()
+    s_bad[b_live * G + 2, 100] = 0x7FC0
+    bad = pair.audit(dm["offsets"], scores_to_device(s_bad, w), dm["rewards"], dm["p"],
+                     w.design_seed, 3, R, meta.gmax, nv=meta.nv)
+    torch.cuda.synchronize()
+    assert int(bad["status"].item()) & pair.ST_NONFINITE
+
+
 def _exact_expected_mse(K, r, p):
     """Prop. 1 trace, E||g^ - g_pair||^2 under independent Bernoulli vertices,
     from the Gram matrix K = S S^T (fp64)."""
@@ -576,11 +633,20 @@ def _exact_expected_mse(K, r, p):
     return tot / (M * M)
 
 
-@pytest.mark.timeout(400)
+@pytest.mark.timeout(600)
 def test_audit_full_size():
-    """The audit workload at full size (B=256, G=16, D=65536, R=4096): two
-    sampled prompts against the oracle with every replicate, and for all
-    prompts the Monte-Carlo MSE against its exact expectation (Prop. 1)."""
+    """The audit workload at full size (B=256, G=16, D=65536, R=4096), in the
+    launch the bench times.
+      1. The explicit-edge oracle on 16 prompts with unequal rewards, spread
+         over the batch (and so over the XCD ranges and column slices), every
+         replicate.
+      2. Every e_r of every prompt (256 x 4096) against delta_r K delta_r^T,
+         with the deviations delta_r = A~^(r) - a from the oracle's design
+         draw and coefficient fold and K = S S^T in fp64 on the host (the
+         Gram identity pinned against the explicit oracle); prompts with equal
+         rewards must give exact zeros.
+      3. For all prompts the Monte-Carlo MSE against its exact expectation
+         (Prop. 1)."""
     w = wl.WORKLOADS["audit"]
     meta = wl.host_meta(w)
     log(f"audit full size B={meta.B} D={w.D} R={w.R}")
@@ -593,26 +659,59 @@ def test_audit_full_size():
     mse = got["mse"].cpu().numpy()
     reps = got["rep_sqerr"].cpu().numpy().astype(np.float64)
     assert np.allclose(mse, reps.mean(axis=1), rtol=1e-6, atol=0)
-    # oracle: one prompt with every replicate, a second on a replicate window
-    b = 3
-    o0, o1 = meta.offsets[b], meta.offsets[b + 1]
-    log(f"  oracle prompt {b}, all replicates")
-    want = oracle.audit(np.array([0, o1 - o0]), scores_to_host(sd[o0:o1]), meta.rewards[o0:o1],
-                        meta.p[o0:o1], w.design_seed, 0, w.R, prompt_id=[b])
-    sub = {"mse": got["mse"][b:b + 1], "bias_norm": got["bias_norm"][b:b + 1],
-           "rep_sqerr": got["rep_sqerr"][b:b + 1], "edge_count": got["edge_count"][b:b + 1],
-           "status": got["status"]}
-    _check_audit(sub, want, f"prompt {b}")
-    b, r0, nr = 200, 2048, 256
-    o0, o1 = meta.offsets[b], meta.offsets[b + 1]
-    log(f"  oracle prompt {b}, replicates {r0}..{r0 + nr - 1}")
-    want = oracle.audit(np.array([0, o1 - o0]), scores_to_host(sd[o0:o1]), meta.rewards[o0:o1],
-                        meta.p[o0:o1], w.design_seed, r0, nr, prompt_id=[b])
-    assert np.array_equal(got["edge_count"][b, r0:r0 + nr].cpu().numpy(), want["edge_count"][0])
-    e_err = rel_l2(reps[b, r0:r0 + nr], want["rep_sqerr"][0])
-    log(f"  prompt {b} window: rep_sqerr rel L2 {e_err:.2e}")
-    assert e_err <= BF16_TOL
-    # every prompt: MC MSE within 6 standard errors of the exact expectation
+    G = 16
+    rew = meta.rewards.reshape(meta.B, G)
+    live = np.ptp(rew, axis=1) > 0
+    log(f"  {live.sum()} prompts with unequal rewards, {meta.B - live.sum()} with equal rewards")
+    assert 0 < live.sum() < meta.B
+
+    # 1. explicit oracle, 16 live prompts, all replicates, one call
+    live_ids = np.flatnonzero(live)
+    pick = live_ids[np.unique(np.linspace(0, live_ids.size - 1, 16).round().astype(int))]
+    assert pick.size == 16 and pick[0] == live_ids[0] and pick[-1] == live_ids[-1]
+    log(f"  oracle on prompts {pick.tolist()}, all replicates")
+    rows = np.concatenate([np.arange(meta.offsets[b], meta.offsets[b + 1]) for b in pick])
+    sub_off = np.arange(pick.size + 1, dtype=np.int64) * G
+    want = oracle.audit(sub_off, scores_to_host(sd.index_select(0, torch.from_numpy(rows).to(DEV))),
+                        meta.rewards[rows], meta.p[rows], w.design_seed, 0, w.R,
+                        prompt_id=pick)
+    assert np.all(np.linalg.norm(want["rep_sqerr"], axis=1) > 0)
+    pk = torch.from_numpy(pick).to(DEV)
+    sub = {k: got[k].index_select(0, pk) for k in ("mse", "bias_norm", "rep_sqerr", "edge_count")}
+    sub["status"] = got["status"]
+    _check_audit(sub, want, "16 live prompts")
+    for q, b in enumerate(pick):
+        e_b = rel_l2(reps[b], want["rep_sqerr"][q])
+        assert e_b <= BF16_TOL, f"prompt {b}: rep_sqerr rel L2 {e_b:.2e}"
+
+    # 2. every replicate of every prompt through the Gram identity
+    log("  all prompts: oracle draws and folds, K = S S^T on the host")
+    od = oracle.design_inclusion(meta.offsets, meta.p, w.design_seed, 0, w.R, meta.gmax)
+    assert np.array_equal(got["edge_count"].cpu().numpy(), od["edge_count"].T)
+    a_full, _ = oracle.pair_coeffs(meta.offsets, meta.rewards)
+    delta = np.empty((w.R, meta.nv), dtype=np.float64)
+    for r in range(w.R):
+        c_r, _ = oracle.pair_coeffs(meta.offsets, meta.rewards, od["mask"][r], od["pi"])
+        delta[r] = c_r - a_full
+    delta = delta.reshape(w.R, meta.B, G)
+    s_host = scores_to_host(sd)
+    e_gram = np.empty((meta.B, w.R), dtype=np.float64)
+    for b in range(meta.B):
+        sb = (s_host[b * G:(b + 1) * G].astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+        K = sb @ sb.T
+        db = delta[:, b, :]
+        e_gram[b] = np.einsum("ri,ij,rj->r", db, K, db)
+    del s_host
+    assert np.all(e_gram[~live] == 0.0) and np.all(reps[~live] == 0.0)
+    assert np.all(mse[~live] == 0.0) and np.all(got["bias_norm"].cpu().numpy()[~live] == 0.0)
+    per = np.array([rel_l2(reps[b], e_gram[b]) for b in live_ids])
+    tot = rel_l2(reps[live], e_gram[live])
+    log(f"  every e_r vs Gram form: rel L2 {tot:.2e}, worst prompt {per.max():.2e} "
+        f"(prompt {live_ids[per.argmax()]})")
+    assert tot <= BF16_TOL
+    assert per.max() <= BF16_TOL
+
+    # 3. every prompt: MC MSE within 6 standard errors of the exact expectation
     S = sd.view(meta.B, 16, w.D).double()
     K = torch.bmm(S, S.transpose(1, 2).contiguous()).cpu().numpy()
     z = []

@@ -19,9 +19,17 @@ import torch
 
 import oracle
 import paper_2608_11368_amd as pair
-from tests.gpu_util import DEV, log, rel_l2
+from tests.gpu_util import DEV, log
+from tests.gpu_util import rel_l2 as _rel_l2
 
 pytestmark = pytest.mark.gpu
+
+
+def rel_l2(got, want):
+    # A random case may draw only saturated prompts (an all-zero reference);
+    # exact zeros are then required, and checked again where it matters.
+    return _rel_l2(got, want, zero_ok=True)
+
 
 FP32_TOL = 1e-5
 BF16_TOL = 2e-3
