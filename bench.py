@@ -404,8 +404,9 @@ def time_wgrad_configs(pair, stream, wl, dev, coeff, out, scores, off, rew, p, m
                        status, B, nv, G, D, w):
     """The weighted-gradient stream beyond the headline workload: the b128
     batch-mean reduce mode (score bytes are nearly all its traffic), and the
-    per-prompt mode on the Qwen3-shaped slice (B=64, G=8, D=2^26, 68.7 GB of
-    bf16 scores) and on the ragged workload (B=512, G_b ~ U{2..64}, D=2^18).
+    per-prompt and batch-mean modes on the Qwen3-shaped slice (B=64, G=8,
+    D=2^26, 68.7 GB of bf16 scores) and on the ragged workload (B=512,
+    G_b ~ U{2..64}, D=2^18).
     GB/s of algorithmic bytes (nonzero score rows, coefficients, offsets,
     output), kernel timed alone with events on the launch stream."""
     import torch
@@ -437,13 +438,21 @@ def time_wgrad_configs(pair, stream, wl, dev, coeff, out, scores, off, rew, p, m
             reps = 3 if wk.D > (1 << 24) else 10
             ms = _event_ms(stream, lambda: pair.pair_weighted_grad(
                 meta.B, meta.nv, o_k, s_k, c_k, out_k, 0, status, stream), reps)
+            del out_k
+            mean_k = torch.empty(wk.D, dtype=torch.float32, device=dev)
+            ms_mean = _event_ms(stream, lambda: pair.pair_weighted_grad(
+                meta.B, meta.nv, o_k, s_k, c_k, mean_k, 1, status, stream), reps)
         nz = int(torch.count_nonzero(c_k).item())
         alg = nz * wk.D * 2 + meta.nv * 4 + (meta.B + 1) * 8 + meta.B * wk.D * 4
         res[name] = {"B": meta.B, "nv": meta.nv, "D": wk.D, "rows_nonzero": nz,
                      "ms": round(ms, 4), "GBps": round(alg / ms / 1e6, 1),
                      "score_only_GBps": round(nz * wk.D * 2 / ms / 1e6, 1),
                      "frac": round(alg / ms / 1e6 / HBM_PEAK_GBPS, 4)}
-        del s_k, out_k
+        alg_mean = nz * wk.D * 2 + meta.nv * 4 + (meta.B + 1) * 8 + wk.D * 4
+        res[name + "_batch_mean"] = {"ms": round(ms_mean, 4),
+                                     "GBps": round(alg_mean / ms_mean / 1e6, 1),
+                                     "frac": round(alg_mean / ms_mean / 1e6 / HBM_PEAK_GBPS, 4)}
+        del s_k, mean_k
         torch.cuda.empty_cache()
     if int(status.item()) != 0:
         raise RuntimeError(f"device status {int(status.item())} in the gradient configurations")

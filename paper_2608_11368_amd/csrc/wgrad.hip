@@ -168,82 +168,144 @@ __global__ __launch_bounds__(kThreads) void wgrad_kernel(
   }
 }
 
-// Batch mean over prompts, out[d] = (1/B) sum_b g_b[d]: every packed row
-// offsets[0] .. offsets[B]-1 is summed flat in ascending order (the prompts
-// partition that range), so one workgroup owns 1024 columns of the output and
-// sweeps all rows; a lane keeps up to kMeanBatch rows of its 4 columns in
-// flight.  Workgroup 0 also checks that the offsets are monotone.
-constexpr int kMeanBatch = 16;
+// Batch mean over prompts, out[d] = (1/B) sum_b g_b[d]: the prompts
+// partition the packed rows offsets[0] .. offsets[B]-1, so the mean is one
+// flat sum over those rows.  A workgroup owns 1024 output columns (4 per
+// thread of a 256-thread row group) and RG row groups.  The rows are taken in
+// chunks of kMeanChunk: the chunk's nonzero coefficients are listed in LDS
+// in ascending row order (a ballot prefix count per wave, the waves in
+// order), the list is split into RG contiguous parts, and row group q sums
+// part q with kMeanBatch rows in flight per lane and the next batch's loads
+// issued before the current batch's FMAs.  The groups' partial sums are added
+// in LDS in group order at the end, so the result is deterministic for a
+// given D (RG depends only on D).  Workgroup 0 also checks that the offsets
+// are monotone.
+constexpr int kMeanBatch = 8;
+constexpr int kMeanChunk = 2048;
 
-template <bool BF16>
-__global__ __launch_bounds__(kThreads) void wgrad_mean_kernel(
+template <bool BF16, int RG>
+__global__ __launch_bounds__(kThreads * RG) void wgrad_mean_kernel(
     int64_t B, int64_t nv, const int64_t* __restrict__ offsets,
     const unsigned char* __restrict__ scores, int64_t row_bytes, const float* __restrict__ coeff,
     float* __restrict__ out, int64_t D, int vec_out, int32_t* d_status) {
   using T = PieceTraits<BF16>;
-  const int lane = threadIdx.x & (kWave - 1);
+  constexpr int kN = kThreads * RG;
+  constexpr int kWaves = kN / kWave;
+  __shared__ int32_t list_row[kMeanChunk];     // row index relative to the chunk start
+  __shared__ float list_c[kMeanChunk];
+  __shared__ int32_t wcount[kWaves];
+  __shared__ float part[RG > 1 ? RG - 1 : 1][kThreads][kPieceCols];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int grp = tid / kThreads;
+  const int t = tid - grp * kThreads;
   const int64_t lo = offsets[0], hi = offsets[B];
   if (blockIdx.x == 0) {
     bool bad = false;
-    for (int64_t b = threadIdx.x; b < B; b += kThreads) {
+    for (int64_t b = tid; b < B; b += kN) {
       const int64_t x = offsets[b], y = offsets[b + 1];
       bad |= x < 0 || y < x || y > nv;
     }
     if (bad) raise_status(d_status, PAIR_ST_BAD_GROUP);
   }
   if (lo < 0 || hi < lo || hi > nv) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) raise_status(d_status, PAIR_ST_BAD_GROUP);
+    if (blockIdx.x == 0 && tid == 0) raise_status(d_status, PAIR_ST_BAD_GROUP);
     return;
   }
 
-  const int64_t c0 = (int64_t)blockIdx.x * (kThreads * kPieceCols) + threadIdx.x * kPieceCols;
+  const int64_t c0 = (int64_t)blockIdx.x * (kThreads * kPieceCols) + t * kPieceCols;
   const bool full = c0 + kPieceCols <= D;
-  const bool part = !full && c0 < D;
+  const bool part_cols = !full && c0 < D;
   float acc[kPieceCols] = {0.0f, 0.0f, 0.0f, 0.0f};
   const unsigned char* col = scores + c0 * T::kBytes;
 
-  for (int64_t w0 = lo; w0 < hi; w0 += kWave) {
-    const float cv = (w0 + lane < hi) ? coeff[w0 + lane] : 0.0f;
-    uint64_t nz = __ballot(cv != 0.0f);
-    while (nz != 0ull) {
-      int64_t roff[kMeanBatch];
-      float cs[kMeanBatch];
-      int n = 0;
-#pragma unroll
-      for (int s = 0; s < kMeanBatch; ++s) {
-        roff[s] = 0;
-        cs[s] = 0.0f;
-        if (nz != 0ull) {
-          const int j = __ffsll((unsigned long long)nz) - 1;
-          nz &= nz - 1ull;
-          roff[s] = (w0 + j) * row_bytes;
-          cs[s] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cv), j));
-          n = s + 1;
-        }
+  for (int64_t r0 = lo; r0 < hi; r0 += kMeanChunk) {
+    const int64_t nrows = hi - r0 < kMeanChunk ? hi - r0 : kMeanChunk;
+    // List the chunk's nonzero coefficients in ascending row order.
+    int32_t base = 0;
+    for (int k0 = 0; k0 < nrows; k0 += kN) {
+      const int k = k0 + tid;
+      const float cv = k < nrows ? coeff[r0 + k] : 0.0f;
+      const uint64_t m = __ballot(cv != 0.0f);
+      if (lane == 0) wcount[wave] = __popcll(m);
+      __syncthreads();
+      int32_t off = base, tot = 0;
+      for (int w = 0; w < kWaves; ++w) {
+        off += w < wave ? wcount[w] : 0;
+        tot += wcount[w];
       }
-      if (full) {
-        typename T::Vec v[kMeanBatch];
+      if (cv != 0.0f) {
+        const int at = off + __popcll(m & ((1ull << lane) - 1ull));
+        list_row[at] = k;
+        list_c[at] = cv;
+      }
+      base += tot;
+      __syncthreads();
+    }
+    // Row group grp sums list entries [e0, e1).
+    const int n = base;
+    const int e0 = (int)((int64_t)n * grp / RG), e1 = (int)((int64_t)n * (grp + 1) / RG);
+    const unsigned char* cbase = col + r0 * row_bytes;
+    if (full) {
+      typename T::Vec va[kMeanBatch], vb[kMeanBatch];
+      float ca[kMeanBatch], cb[kMeanBatch];
+      auto issue = [&](int e, typename T::Vec (&v)[kMeanBatch], float (&c)[kMeanBatch]) {
+#pragma unroll
+        for (int s = 0; s < kMeanBatch; ++s) {
+          c[s] = 0.0f;
+          if (e + s < e1) {
+            c[s] = list_c[e + s];
+            v[s] = T::load(cbase + (int64_t)list_row[e + s] * row_bytes);
+          }
+        }
+      };
+      auto consume = [&](int e, const typename T::Vec (&v)[kMeanBatch], const float (&c)[kMeanBatch]) {
 #pragma unroll
         for (int s = 0; s < kMeanBatch; ++s)
-          if (s < n) v[s] = T::load(col + roff[s]);
-#pragma unroll
-        for (int s = 0; s < kMeanBatch; ++s)
-          if (s < n) T::fma(acc, cs[s], v[s]);
-      } else if (part) {
-        for (int s = 0; s < n; ++s)
-          for (int e = 0; e < kPieceCols; ++e)
-            if (c0 + e < D)
-              acc[e] = __builtin_fmaf(cs[s], T::elem(scores + roff[s], c0 + e), acc[e]);
+          if (e + s < e1) T::fma(acc, c[s], v[s]);
+      };
+      int e = e0;
+      if (e < e1) issue(e, va, ca);
+      while (e < e1) {
+        const int en = e + kMeanBatch;
+        if (en < e1) issue(en, vb, cb);
+        consume(e, va, ca);
+        if (en >= e1) break;
+        const int em = en + kMeanBatch;
+        if (em < e1) issue(em, va, ca);
+        consume(en, vb, cb);
+        e = em;
+      }
+    } else if (part_cols) {
+      for (int e = e0; e < e1; ++e) {
+        const float cs = list_c[e];
+        const unsigned char* row = scores + (r0 + list_row[e]) * row_bytes;
+        for (int q = 0; q < kPieceCols; ++q)
+          if (c0 + q < D) acc[q] = __builtin_fmaf(cs, T::elem(row, c0 + q), acc[q]);
       }
     }
+    __syncthreads();   // the list is rebuilt for the next chunk
   }
 
+  if (RG > 1) {
+    if (grp > 0) {
+#pragma unroll
+      for (int q = 0; q < kPieceCols; ++q) part[grp - 1][t][q] = acc[q];
+    }
+    __syncthreads();
+    if (grp > 0) return;
+#pragma unroll
+    for (int g2 = 1; g2 < RG; ++g2)
+#pragma unroll
+      for (int q = 0; q < kPieceCols; ++q) acc[q] += part[g2 - 1][t][q];
+  }
   const float fb = (float)B;
   if (full && vec_out) {
     store_nt16(out + c0, acc[0] / fb, acc[1] / fb, acc[2] / fb, acc[3] / fb);
-  } else if (full || part) {
-    for (int e = 0; e < kPieceCols; ++e)
-      if (c0 + e < D) out[c0 + e] = acc[e] / fb;
+  } else if (full || part_cols) {
+    for (int q = 0; q < kPieceCols; ++q)
+      if (c0 + q < D) out[c0 + q] = acc[q] / fb;
   }
 }
 
@@ -259,13 +321,19 @@ int launch_wgrad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D, const
   if (reduce) {
     const int64_t grid = (D + kThreads * kPieceCols - 1) / (kThreads * kPieceCols);
     if (grid > 0x7fffffffLL) return PAIR_ERANGE;
+    // Row groups per workgroup: enough that the grid holds about 8 waves per
+    // SIMD of the chip (4 row groups at most, one 1024-thread workgroup).
+    const int64_t simds = 4 * (int64_t)device_cu_count();
+    const int rg = grid * 4 >= 8 * simds ? 1 : (grid * 8 >= 8 * simds ? 2 : 4);
+#define PAIR_MEAN(BF, RG_)                                                                       \
+  hipLaunchKernelGGL((wgrad_mean_kernel<BF, RG_>), dim3((unsigned)grid), dim3(kThreads * RG_), 0, \
+                     stream, B, nv, offsets, s, row_bytes, coeff, out, D, vec_out, d_status)
     if (bf16) {
-      hipLaunchKernelGGL(wgrad_mean_kernel<true>, dim3((unsigned)grid), dim3(kThreads), 0, stream,
-                         B, nv, offsets, s, row_bytes, coeff, out, D, vec_out, d_status);
+      if (rg == 1) PAIR_MEAN(true, 1); else if (rg == 2) PAIR_MEAN(true, 2); else PAIR_MEAN(true, 4);
     } else {
-      hipLaunchKernelGGL(wgrad_mean_kernel<false>, dim3((unsigned)grid), dim3(kThreads), 0,
-                         stream, B, nv, offsets, s, row_bytes, coeff, out, D, vec_out, d_status);
+      if (rg == 1) PAIR_MEAN(false, 1); else if (rg == 2) PAIR_MEAN(false, 2); else PAIR_MEAN(false, 4);
     }
+#undef PAIR_MEAN
     return hipGetLastError() == hipSuccess ? PAIR_OK : PAIR_EHIP;
   }
   const int64_t tile = (int64_t)kThreads * kPieceCols * (bf16 ? 4 : 2);

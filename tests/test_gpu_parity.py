@@ -378,19 +378,21 @@ def test_weighted_grad_mean_edge_cases():
         assert bool((zero == 0).all())
 
 
-def test_weighted_grad_mean_full_size_sampled():
-    """b128 at full size in batch-mean mode, sampled columns against the oracle."""
-    w = wl.WORKLOADS["b128"]
+@pytest.mark.parametrize("name", ["b128", "ragged", "qwen3"])
+def test_weighted_grad_mean_full_size_sampled(name):
+    """The workload at full size in batch-mean mode (one, two or four row
+    groups per workgroup, the ragged workload's 16,961 rows in several LDS
+    chunks), a column in every 1024-column workgroup slice against the
+    oracle, and every column against the mean of the per-prompt rows."""
+    w = wl.WORKLOADS[name]
     meta = wl.host_meta(w)
-    log(f"batch mean full size b128 nv={meta.nv} D={w.D}")
+    log(f"batch mean full size {name} nv={meta.nv} D={w.D}")
     dm = upload_meta(meta)
     sd = wl.device_scores(w, meta.nv, DEV)
     d, c, g = _chain_gpu(meta, dm, sd, w.design_seed, meta.gmax)
     gm = pair.weighted_grad(dm["offsets"], sd, c["coeff"], nv=meta.nv, reduce=True)
     torch.cuda.synchronize()
-    rng = np.random.default_rng(5)
-    cols = np.unique(np.concatenate([rng.choice(w.D, 2048, replace=False),
-                                     np.arange(w.D - 16, w.D)]))
+    cols = tile_columns(w.D, 1024, np.random.default_rng(5))
     ci = torch.from_numpy(cols).to(DEV)
     s_host = scores_to_host(sd.index_select(1, ci))
     _, est, _ = _chain_oracle(meta, s_host, w.design_seed, meta.gmax)
@@ -398,7 +400,8 @@ def test_weighted_grad_mean_full_size_sampled():
     log(f"  sampled mean rel L2 = {err:.3e}")
     assert err <= BF16_TOL
     # the batch mean of the per-prompt rows, on every column (fp32 rounding only)
-    assert rel_l2(gm["out"].double().cpu().numpy(), g["out"].double().mean(0).cpu().numpy()) <= 1e-6
+    per_prompt_mean = torch.mean(g["out"], dim=0, dtype=torch.float64).cpu().numpy()
+    assert rel_l2(gm["out"].double().cpu().numpy(), per_prompt_mean) <= 1e-6
     del sd, g, gm
     torch.cuda.empty_cache()
 
