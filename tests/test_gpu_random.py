@@ -143,7 +143,24 @@ def test_random_gradient_chain(case_id):
         if not np.any(est[b]):
             assert np.all(out[b] == 0.0), f"prompt {b} must be exactly zero"
     gm = pair.weighted_grad(off, c["dev"], co["coeff"], nv=nv, reduce=True)["out"].cpu().numpy()
-    assert np.isfinite(gm).all() and rel_l2(gm, est.mean(axis=0)) <= tol
+    assert np.isfinite(gm).all()
+    # The batch mean of a few columns can cancel far below its summands (a
+    # single column at 1/680 of them in one case), and fp32 coefficients and
+    # accumulation then cannot reach a bound relative to the result itself.
+    # Its error is measured against the larger of the result and 1/100 of the
+    # summands' magnitude sum_i |c_i| |s_i| / B (the fp32 summation bound).
+    want_m = est.mean(axis=0)
+    host = np.nan_to_num(np.asarray(c["host"], dtype=np.float64) if not c["bf16"] else
+                         (c["host"].astype(np.uint32) << 16).view(np.float32).astype(np.float64))
+    mag = np.abs(want_c) @ np.abs(np.where(want_c[:, None] != 0.0, host, 0.0)) / B
+    scale = max(np.linalg.norm(want_m), np.linalg.norm(mag) / 100.0)
+    if scale == 0.0:                                   # every prompt saturated: exact zeros
+        assert np.all(gm == 0.0)
+        return
+    err_m = np.linalg.norm(gm - want_m) / scale
+    log(f"  batch mean error {err_m:.2e} "
+        f"(result / summands {np.linalg.norm(want_m) / np.linalg.norm(mag):.2e})")
+    assert err_m <= tol
 
 
 @pytest.mark.parametrize("case_id", range(16))
