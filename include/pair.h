@@ -50,6 +50,8 @@ extern "C" {
 #define PAIR_EALIGN (-4)     /* scores base or row stride not 16-byte aligned   */
 #define PAIR_EHIP (-5)       /* a HIP launch or runtime call failed             */
 #define PAIR_EWORKSPACE (-6) /* workspace missing, misaligned or too small      */
+#define PAIR_ESCRATCH (-7)   /* one prompt's audit needs more than the static
+                                scratch of pair_audit_noalloc                  */
 
 /* Score dtypes. */
 #define PAIR_F32 0
@@ -350,6 +352,30 @@ int pair_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int6
                const float* p, const float* pi_w, uint64_t seed, int64_t rep0, int64_t R,
                double* mse, double* bias_norm, float* rep_sqerr, int32_t* edge_count,
                void* workspace, size_t ws_bytes, int32_t* d_status, void* stream);
+
+/*
+ * pair_audit_noalloc -- pair_audit for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  The arguments are pair_audit's without the workspace.
+ * Its workspace is instead a static device array of the library,
+ * PAIR_AUDIT_SCRATCH_BYTES (64 MiB) on each GPU it runs on, held from its
+ * first call on that GPU until the process ends.  The prompts are audited in
+ * consecutive chunks whose pair_audit_workspace_bytes fits that array, so the
+ * outputs are bitwise those of pair_audit with the same arguments (the audit
+ * workload's shape, G = 16, D = 65536, R = 4096, takes about 80 prompts per
+ * chunk).  If a single prompt needs more than the array it returns
+ * PAIR_ESCRATCH and enqueues nothing.  The call allocates nothing and calls no
+ * allocating routine.  Every call on one GPU uses that GPU's one array, which
+ * keeps the last call's contents: calls ordered on one stream are safe, but
+ * calls that overlap on one GPU (other streams, other host threads) race and
+ * their outputs are undefined.
+ */
+#define PAIR_AUDIT_SCRATCH_BYTES ((size_t)64 << 20)
+int pair_audit_noalloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                       const void* scores, int32_t dtype, int64_t ld, const float* rewards,
+                       const float* p, const float* pi_w, uint64_t seed, int64_t rep0, int64_t R,
+                       double* mse, double* bias_norm, float* rep_sqerr, int32_t* edge_count,
+                       int32_t* d_status, void* stream);
 
 /*
  * pair_audit_rule -- pair_audit replaying the estimator under an edge-weight

@@ -41,6 +41,8 @@ DESIGN_PAIR = 0
 DESIGN_POINTWISE = 1
 DESIGN_UNIFORM = 2
 GMAX_LIMIT = 64
+# Bytes of the static device scratch that pair_audit_noalloc uses as its workspace.
+AUDIT_SCRATCH_BYTES = 64 << 20
 
 RULE_HT = 0
 RULE_UNWEIGHTED = 1
@@ -52,8 +54,8 @@ RULE_MARGINAL = 5
 EXPORTED = ("pair_design_coeffs", "pair_design_alloc", "pair_cps_fit", "pair_cps_draw", "pair_design_inclusion", "pair_edge_coeffs", "pair_edge_coeffs_rule",
             "pair_weighted_grad", "pair_audit_workspace_bytes", "pair_audit", "pair_audit_rule",
             "pair_audit_exact_workspace_bytes", "pair_audit_exact",
-            "pair_audit_direction_workspace_bytes", "pair_audit_direction", "pair_strerror",
-            "pair_version")
+            "pair_audit_direction_workspace_bytes", "pair_audit_direction", "pair_audit_noalloc",
+            "pair_strerror", "pair_version")
 
 
 class PairError(RuntimeError):
@@ -110,6 +112,9 @@ def lib() -> ctypes.CDLL:
         L.pair_audit.argtypes = [i64, i64, i32, P, i64, P, i32, i64, P, P, P, u64, i64, i64,
                                  P, P, P, P, P, ctypes.c_size_t, P, P]
         L.pair_audit.restype = ctypes.c_int
+        L.pair_audit_noalloc.argtypes = [i64, i64, i32, P, i64, P, i32, i64, P, P, P, u64, i64,
+                                         i64, P, P, P, P, P, P]
+        L.pair_audit_noalloc.restype = ctypes.c_int
         L.pair_strerror.argtypes = [ctypes.c_int]
         L.pair_strerror.restype = ctypes.c_char_p
         L.pair_version.argtypes = []
@@ -286,6 +291,21 @@ def pair_audit_rule(B, nv, gmax, offsets, scores, rewards, p, pi_w, rule, wmax, 
         _dev(edge_count, "edge_count", torch.int32, B * R, True),
         ws, workspace.numel(), _dev(d_status, "d_status", torch.int32, 1, True),
         _stream(stream)), _name)
+
+
+def pair_audit_noalloc(B, nv, gmax, offsets, scores, rewards, p, pi_w, seed, rep0, R, mse,
+                       bias_norm, rep_sqerr=None, edge_count=None, d_status=None, stream=None):
+    """pair_audit with the library's static device scratch as its workspace."""
+    sp, code, ld, D = _scores_arg(scores)
+    _rc(lib().pair_audit_noalloc(
+        B, nv, gmax, _dev(offsets, "offsets", torch.int64, B + 1), D, sp, code, ld,
+        _dev(rewards, "rewards", torch.float32, nv), _dev(p, "p", torch.float32, nv),
+        _dev(pi_w, "pi_w", torch.float32, B * gmax * gmax, True),
+        ctypes.c_uint64(seed & ((1 << 64) - 1)), rep0, R,
+        _dev(mse, "mse", torch.float64, B), _dev(bias_norm, "bias_norm", torch.float64, B),
+        _dev(rep_sqerr, "rep_sqerr", torch.float32, B * R, True),
+        _dev(edge_count, "edge_count", torch.int32, B * R, True),
+        _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_audit_noalloc")
 
 
 def pair_audit_direction_workspace_bytes(B, gmax, D, R) -> int:

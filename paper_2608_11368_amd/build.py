@@ -13,7 +13,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libpair.so")
-SOURCES = ["api.hip", "design.hip", "coeffs.hip", "wgrad.hip", "audit.hip", "exact.hip", "alloc.hip", "cps.hip"]
+SOURCES = ["api.hip", "design.hip", "coeffs.hip", "wgrad.hip", "audit.hip", "exact.hip", "alloc.hip",
+           "cps.hip", "noalloc.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU ops are kept off in all device code.

@@ -152,7 +152,7 @@ int pair_audit_rule(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
       ws_bytes < need)
     return PAIR_EWORKSPACE;
   return pair::launch_audit(B, nv, gmax, offsets, D, scores, ld, rewards, p, pi_w, rule, wmax,
-                            seed, rep0, R,
+                            seed, rep0, 0, R,
                             mse, bias_norm, rep_sqerr, edge_count, workspace, d_status,
                             as_stream(stream));
 }
@@ -267,6 +267,25 @@ int pair_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int6
                          workspace, ws_bytes, d_status, stream);
 }
 
+int pair_audit_noalloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                       const void* scores, int32_t dtype, int64_t ld, const float* rewards,
+                       const float* p, const float* pi_w, uint64_t seed, int64_t rep0, int64_t R,
+                       double* mse, double* bias_norm, float* rep_sqerr, int32_t* edge_count,
+                       int32_t* d_status, void* stream) {
+  int st = check_groups(B, nv, gmax, offsets);
+  if (st) return st;
+  if (dtype != PAIR_BF16) return PAIR_EDTYPE;
+  st = check_scores(scores, dtype, D, ld);
+  if (st) return st;
+  if (rewards == nullptr || p == nullptr || mse == nullptr || bias_norm == nullptr)
+    return PAIR_EINVAL;
+  if (R < 1 || rep0 < 0 || R > kMaxCount || rep0 > kMaxCount) return PAIR_ERANGE;
+  if (pair_audit_workspace_bytes(B, gmax, D, R) == 0) return PAIR_ERANGE;
+  return pair::launch_audit_noalloc(B, nv, gmax, offsets, D, scores, ld, rewards, p, pi_w, seed,
+                                    rep0, R, mse, bias_norm, rep_sqerr, edge_count, d_status,
+                                    as_stream(stream));
+}
+
 const char* pair_strerror(int code) {
   switch (code) {
     case PAIR_OK: return "ok";
@@ -276,10 +295,12 @@ const char* pair_strerror(int code) {
     case PAIR_EALIGN: return "scores base pointer or row stride not 16-byte aligned";
     case PAIR_EHIP: return "HIP launch or runtime error";
     case PAIR_EWORKSPACE: return "workspace missing, misaligned or too small";
+    case PAIR_ESCRATCH:
+      return "one prompt's audit workspace exceeds the no-alloc entry point's static scratch";
     default: return "unknown error code";
   }
 }
 
-int pair_version(void) { return 200; }   // 0.2.0: pair_audit_direction added
+int pair_version(void) { return 300; }   // 0.3.0: pair_audit_noalloc added
 
 }  // extern "C"

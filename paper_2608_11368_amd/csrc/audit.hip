@@ -141,8 +141,8 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
     int64_t B, int64_t nv, int32_t gmax, const int64_t* __restrict__ offsets,
     const float* __restrict__ rewards, const float* __restrict__ p,
     const float* __restrict__ pi_w, int32_t rule, float wmax, uint64_t seed, int64_t rep0,
-    int64_t R, int64_t nwg, int64_t rrows, float* __restrict__ delta, float* __restrict__ dsum,
-    int32_t* __restrict__ edge_count, int32_t* d_status) {
+    int64_t pbase, int64_t R, int64_t nwg, int64_t rrows, float* __restrict__ delta,
+    float* __restrict__ dsum, int32_t* __restrict__ edge_count, int32_t* d_status) {
   constexpr int kWaves = kCoefThreads / kWave;
   __shared__ __align__(16) float W[KP * KP];     // rule weight x (r_i - r_j), zero on and past G
   __shared__ __align__(16) float V[KP * KP];     // 1/rho_ij (self-normalised denominator)
@@ -205,7 +205,8 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
   if (valid) {
     const uint64_t rg = (uint64_t)(rep0 + rloc);
     for (int blk = 0; blk * 4 < g; ++blk) {
-      const Philox4x64 x = philox4x64_10(rg, (uint64_t)b, (uint64_t)blk, 0ull, seed, 0ull);
+      const Philox4x64 x =
+          philox4x64_10(rg, (uint64_t)(pbase + b), (uint64_t)blk, 0ull, seed, 0ull);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int i = blk * 4 + q;
@@ -907,8 +908,8 @@ int launch_audit_direction(int64_t B, int64_t nv, int32_t gmax, const int64_t* o
   if (grid > 0x7fffffffLL) return PAIR_ERANGE;
 #define PAIR_DIR(KP_)                                                                           \
   hipLaunchKernelGGL(audit_coeffs_kernel<KP_>, dim3((unsigned)grid), dim3(kCoefThreads), 0,      \
-                     stream, B, nv, gmax, offsets, rewards, p, pi_w, rule, wmax, seed, rep0, R,  \
-                     A.nwg, A.rrows, delta, dsum, nullptr, d_status);                           \
+                     stream, B, nv, gmax, offsets, rewards, p, pi_w, rule, wmax, seed, rep0, 0,  \
+                     R, A.nwg, A.rrows, delta, dsum, nullptr, d_status);                        \
   if (hipGetLastError() != hipSuccess) return PAIR_EHIP;                                        \
   hipLaunchKernelGGL(audit_cosine_kernel<KP_>, dim3((unsigned)grid), dim3(kCosThreads), 0,       \
                      stream, B, nv, gmax, offsets, rewards, R, A.nwg, A.rrows, delta, gram,       \
@@ -929,8 +930,8 @@ int launch_audit_direction(int64_t B, int64_t nv, int32_t gmax, const int64_t* o
 int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
                  const void* scores, int64_t ld, const float* rewards, const float* p,
                  const float* pi_w, int32_t rule, float wmax, uint64_t seed, int64_t rep0,
-                 int64_t R, double* mse, double* bias_norm, float* rep_sqerr, int32_t* edge_count,
-                 void* workspace, int32_t* d_status, hipStream_t stream) {
+                 int64_t pbase, int64_t R, double* mse, double* bias_norm, float* rep_sqerr,
+                 int32_t* edge_count, void* workspace, int32_t* d_status, hipStream_t stream) {
   const AuditLayout L = audit_layout(B, gmax, D, R);
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   float* delta = reinterpret_cast<float*>(ws + L.delta_off);
@@ -950,8 +951,8 @@ int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, in
     return PAIR_ERANGE;
 #define PAIR_AUDIT_COEFFS(KP_)                                                                  \
   hipLaunchKernelGGL(audit_coeffs_kernel<KP_>, dim3((unsigned)coef_grid), dim3(kCoefThreads), 0, \
-                     stream, B, nv, gmax, offsets, rewards, p, pi_w, rule, wmax, seed, rep0, R,  \
-                     L.nwg, L.rrows, delta, dsum, edge_count, d_status)
+                     stream, B, nv, gmax, offsets, rewards, p, pi_w, rule, wmax, seed, rep0,     \
+                     pbase, R, L.nwg, L.rrows, delta, dsum, edge_count, d_status)
   switch (L.ks) {
     case 1: PAIR_AUDIT_COEFFS(16); break;
     case 2: PAIR_AUDIT_COEFFS(32); break;

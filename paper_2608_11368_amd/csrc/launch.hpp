@@ -31,12 +31,22 @@ int launch_wgrad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D, const
 
 size_t audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R);
 
+// Prompt b of the call is prompt pbase + b of the generator's counter (its
+// design draws are those of that prompt index); 0 for a whole batch.
 int launch_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
                  const void* scores, int64_t ld, const float* rewards, const float* p,
                  const float* pi_w, int32_t rule, float wmax, uint64_t seed, int64_t rep0,
-                 int64_t R, double* mse,
-                 double* bias_norm, float* rep_sqerr, int32_t* edge_count, void* workspace,
-                 int32_t* d_status, hipStream_t stream);
+                 int64_t pbase, int64_t R, double* mse, double* bias_norm, float* rep_sqerr,
+                 int32_t* edge_count, void* workspace, int32_t* d_status, hipStream_t stream);
+
+// pair_audit with the library's static scratch as the workspace, the prompts
+// in chunks that fit it (PAIR_ESCRATCH if one prompt does not).
+int64_t audit_noalloc_chunk(int64_t B, int32_t gmax, int64_t D, int64_t R);
+int launch_audit_noalloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
+                         const void* scores, int64_t ld, const float* rewards, const float* p,
+                         const float* pi_w, uint64_t seed, int64_t rep0, int64_t R, double* mse,
+                         double* bias_norm, float* rep_sqerr, int32_t* edge_count,
+                         int32_t* d_status, hipStream_t stream);
 
 int launch_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, const float* p_hat,
                  const float* c_hat, const float* m_hat, const float* budget, float pi_min,

@@ -44,7 +44,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_version_and_strerror():
     assert pair.version() >= 100
-    for code in (0, -1, -2, -3, -4, -5, -6, -99):
+    for code in (0, -1, -2, -3, -4, -5, -6, -7, -99):
         assert isinstance(pair.strerror(code), str) and pair.strerror(code)
 
 
@@ -118,6 +118,27 @@ def test_audit_rejects_bad_arguments_and_sizes_workspace():
     assert call(gmax=80) == -3
     assert call(mse=NULL) == -1
     assert call(s=ODD) == -4
+
+
+def test_audit_noalloc_rejects_bad_arguments_and_oversized_prompts():
+    L = pair.lib()
+    f = L.pair_audit_noalloc
+
+    def call(dt=1, R=4096, gmax=16, mse=FAKE, s=FAKE, D=65536, rep0=0):
+        return f(256, 4096, gmax, FAKE, D, s, dt, D, FAKE, FAKE, NULL, 1, rep0, R, mse, FAKE,
+                 NULL, NULL, NULL, NULL)
+
+    assert call(dt=0) == -2
+    assert call(R=0) == -3
+    assert call(rep0=-1) == -3
+    assert call(gmax=80) == -3
+    assert call(mse=NULL) == -1
+    assert call(s=ODD) == -4
+    # one prompt of 16 candidates, 2^23 score columns and 4096 replicates needs
+    # more workspace than the static scratch holds: rejected before any HIP call
+    assert L.pair_audit_workspace_bytes(1, 16, 1 << 23, 4096) > pair.AUDIT_SCRATCH_BYTES
+    assert call(D=1 << 23) == -7
+    assert "scratch" in pair.strerror(-7)
 
 
 def test_binding_checks_tensors_before_calling():
