@@ -65,6 +65,9 @@ extern "C" {
 #define PAIR_ST_BUDGET 16    /* design: budget below pi_min * sum(c), or an
                                 invalid prefix statistic (p outside [0, 1],
                                 c or m not positive and finite)               */
+#define PAIR_ST_SOLVER 32    /* design: the solver reached its sweep cap or a
+                                search limit before converging; the prompt
+                                fell back to the uniform design               */
 
 /* Edge-weight rules: the estimator variants compared in the paper's audit and
  * ablation tables (Sec. 6, Tables 2, 4, 5; App. A "Naive selection bias" and
@@ -138,7 +141,9 @@ int pair_design_inclusion(int64_t B, int64_t nv, int32_t gmax, const int64_t* of
  *          s.t. sum_i c_i pi_i <= budget_b,  pi_min <= pi_i <= 1
  * (the paper's program in pi_i = e^{-x_i}), solved to the optimum in fp64:
  * exact cyclic coordinate minimisation of the Lagrangian for a multiplier
- * found by bisection.  The budget is spent exactly unless sum_i c_i <=
+ * found by a bracketed false-position search (each coordinate sweep to a
+ * relative change of 1e-13, the budget to 1e-13 relative; the defaults of
+ * pair_design_alloc_ex below).  The budget is spent exactly unless sum_i c_i <=
  * budget_b (then pi = 1).  Vertices with no contrast to any other vertex
  * (all a_ij = 0 and b_i = 0) take pi_min.  The PAIR_DESIGN_POINTWISE design
  * is the same program with a = 0 and b_i = p_i (1 - p_i); PAIR_DESIGN_UNIFORM
@@ -154,15 +159,57 @@ int pair_design_inclusion(int64_t B, int64_t nv, int32_t gmax, const int64_t* of
  *   design         PAIR_DESIGN_*
  *   pi             fp32 [nv] out: continuation probabilities
  *   objective      fp64 [B] out: the PAIR proxy Phi at pi (every design)  (or NULL)
- *   iters          int32 [B] out: coordinate sweeps used                  (or NULL)
+ *   iters          int32 [B] out: coordinate sweeps used (negative: the
+ *                  solver failed and the prompt got the uniform design)   (or NULL)
  * Group sizes 1 <= G_b <= gmax <= 64.  Device status: PAIR_ST_BAD_GROUP;
  * PAIR_ST_BUDGET (budget_b < pi_min sum c: that prompt gets pi = pi_min;
- * invalid statistics: pi = pi_min).
+ * invalid statistics: pi = pi_min); PAIR_ST_SOLVER (see
+ * pair_design_alloc_ex).
  */
 int pair_design_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
                       const float* p_hat, const float* c_hat, const float* m_hat,
                       const float* budget, float pi_min, int32_t design, float* pi,
                       double* objective, int32_t* iters, int32_t* d_status, void* stream);
+
+/*
+ * pair_design_alloc_ex -- pair_design_alloc with the solver settings of the
+ * paper's implementation (App. C "Probability optimization"): a warm start
+ * from the previous step's probabilities, an iteration cap with a fallback to
+ * uniform probabilities of the same expected cost when the solver fails, and
+ * the solver residual per prompt.  pair_design_alloc is this call with
+ * pi_prev = NULL, max_sweeps = 0 and residual = NULL.
+ *
+ *   pi_prev        fp32 [nv] previous probabilities (or NULL: a cold start).
+ *                  They are clipped to [pi_min, 1] (NaN reads as pi_min); the
+ *                  multiplier search starts at the multiplier their KKT
+ *                  conditions imply (the median of A_i / (c_i pi_i^2) over the
+ *                  interior vertices) and brackets the root from there; a
+ *                  start with no interior vertex is a cold start.
+ *   max_sweeps     cap on a prompt's coordinate sweeps over all multipliers
+ *                  (>= 0; 0: 10000).  A prompt that reaches it, or a search
+ *                  limit (400 sweeps per multiplier, 200 multipliers), before
+ *                  converging gets the uniform design clip(budget_b / sum c,
+ *                  pi_min, 1), its iters is minus the sweeps used, and
+ *                  PAIR_ST_SOLVER is set.
+ *   residual       fp64 [B] out: KKT residual of the design's program at the
+ *                  returned fp32 probabilities x (for PAIR_DESIGN_UNIFORM, of
+ *                  the PAIR program).  With g_i = A_i / x_i^2, A_i =
+ *                  sum_{j != i} a_ij / x_j + b_i, and lam the median of
+ *                  g_i / c_i over interior vertices (with none: 0 if the
+ *                  budget is slack, else the largest g_i / c_i at pi_min), it
+ *                  is the largest of |g_i / c_i - lam| (interior), lam - g_i /
+ *                  c_i (at 1), g_i / c_i - lam (at pi_min), all over
+ *                  max_i g_i / c_i, and of |c^T x - budget_b| / budget_b
+ *                  (lam > 0) and the relative overspend.  A vertex is at a
+ *                  bound within 1e-7 relative.                          (or NULL)
+ * Other arguments and device status as pair_design_alloc, plus
+ * PAIR_ST_SOLVER; max_sweeps < 0 returns PAIR_ERANGE.
+ */
+int pair_design_alloc_ex(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                         const float* p_hat, const float* c_hat, const float* m_hat,
+                         const float* budget, float pi_min, int32_t design, const float* pi_prev,
+                         int32_t max_sweeps, float* pi, double* objective, int32_t* iters,
+                         double* residual, int32_t* d_status, void* stream);
 
 /*
  * pair_cps_fit -- fixed-size continuation design (paper App. B "Fixed-size

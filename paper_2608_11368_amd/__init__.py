@@ -37,6 +37,7 @@ ST_RHO_RANGE = 2
 ST_P_RANGE = 4
 ST_NONFINITE = 8
 ST_BUDGET = 16
+ST_SOLVER = 32
 DESIGN_PAIR = 0
 DESIGN_POINTWISE = 1
 DESIGN_UNIFORM = 2
@@ -51,7 +52,7 @@ RULE_CLIPPED = 3
 RULE_SELFNORM = 4
 RULE_MARGINAL = 5
 
-EXPORTED = ("pair_design_coeffs", "pair_design_alloc", "pair_cps_fit", "pair_cps_draw", "pair_design_inclusion", "pair_edge_coeffs", "pair_edge_coeffs_rule",
+EXPORTED = ("pair_design_coeffs", "pair_design_alloc", "pair_design_alloc_ex", "pair_cps_fit", "pair_cps_draw", "pair_design_inclusion", "pair_edge_coeffs", "pair_edge_coeffs_rule",
             "pair_weighted_grad", "pair_audit_workspace_bytes", "pair_audit", "pair_audit_rule",
             "pair_audit_exact_workspace_bytes", "pair_audit_exact",
             "pair_audit_direction_workspace_bytes", "pair_audit_direction", "pair_audit_noalloc",
@@ -94,6 +95,9 @@ def lib() -> ctypes.CDLL:
         L.pair_audit_exact.restype = ctypes.c_int
         L.pair_design_alloc.argtypes = [i64, i64, i32, P, P, P, P, P, f32, i32, P, P, P, P, P]
         L.pair_design_alloc.restype = ctypes.c_int
+        L.pair_design_alloc_ex.argtypes = [i64, i64, i32, P, P, P, P, P, f32, i32, P, i32, P, P, P,
+                                           P, P, P]
+        L.pair_design_alloc_ex.restype = ctypes.c_int
         L.pair_audit_direction_workspace_bytes.argtypes = [i64, i32, i64, i64]
         L.pair_audit_direction_workspace_bytes.restype = ctypes.c_size_t
         L.pair_audit_direction.argtypes = [i64, i64, i32, P, i64, P, i32, i64, P, P, P, i32, f32,
@@ -208,6 +212,21 @@ def pair_design_alloc(B, nv, gmax, offsets, p_hat, c_hat, m_hat, budget, pi_min,
         _dev(objective, "objective", torch.float64, B, True),
         _dev(iters, "iters", torch.int32, B, True),
         _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_design_alloc")
+
+
+def pair_design_alloc_ex(B, nv, gmax, offsets, p_hat, c_hat, m_hat, budget, pi_min, design,
+                         pi_prev, max_sweeps, pi, objective=None, iters=None, residual=None,
+                         d_status=None, stream=None):
+    _rc(lib().pair_design_alloc_ex(
+        B, nv, gmax, _dev(offsets, "offsets", torch.int64, B + 1),
+        _dev(p_hat, "p_hat", torch.float32, nv), _dev(c_hat, "c_hat", torch.float32, nv),
+        _dev(m_hat, "m_hat", torch.float32, nv, True), _dev(budget, "budget", torch.float32, B),
+        float(pi_min), int(design), _dev(pi_prev, "pi_prev", torch.float32, nv, True),
+        int(max_sweeps), _dev(pi, "pi", torch.float32, nv),
+        _dev(objective, "objective", torch.float64, B, True),
+        _dev(iters, "iters", torch.int32, B, True),
+        _dev(residual, "residual", torch.float64, B, True),
+        _dev(d_status, "d_status", torch.int32, 1, True), _stream(stream)), "pair_design_alloc_ex")
 
 
 def pair_cps_fit(B, nv, gmax, offsets, pi_target, w, n_out=None, pi_joint=None, iters=None,
@@ -506,9 +525,10 @@ def audit_exact(offsets, scores, rewards, p, gmax, pi_w=None, rule=RULE_HT, wmax
 
 @_allocating
 def design_alloc(offsets, p_hat, c_hat, budget, gmax, pi_min=0.08, design=DESIGN_PAIR, m_hat=None,
-                 nv=None, stream=None):
+                 nv=None, pi_prev=None, max_sweeps=0, stream=None):
     """Continuation probabilities of every prompt (fp32 [nv]) with the
-    objective, sweep counts and status."""
+    objective, sweep counts (negative: solver fallback), KKT residual and
+    status; `pi_prev` warm-starts the solver, `max_sweeps` caps it."""
     B = offsets.numel() - 1
     nv = _nv(offsets) if nv is None else nv
     dev = p_hat.device
@@ -516,10 +536,12 @@ def design_alloc(offsets, p_hat, c_hat, budget, gmax, pi_min=0.08, design=DESIGN
         "pi": torch.empty(nv, dtype=torch.float32, device=dev),
         "objective": torch.empty(B, dtype=torch.float64, device=dev),
         "iters": torch.empty(B, dtype=torch.int32, device=dev),
+        "residual": torch.empty(B, dtype=torch.float64, device=dev),
         "status": torch.zeros(1, dtype=torch.int32, device=dev),
     }
-    pair_design_alloc(B, nv, gmax, offsets, p_hat, c_hat, m_hat, budget, pi_min, design, out["pi"],
-                      out["objective"], out["iters"], out["status"], stream)
+    pair_design_alloc_ex(B, nv, gmax, offsets, p_hat, c_hat, m_hat, budget, pi_min, design,
+                         pi_prev, max_sweeps, out["pi"], out["objective"], out["iters"],
+                         out["residual"], out["status"], stream)
     return out
 
 

@@ -190,10 +190,11 @@ int pair_audit_direction(int64_t B, int64_t nv, int32_t gmax, const int64_t* off
                                       d_status, as_stream(stream));
 }
 
-int pair_design_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
-                      const float* p_hat, const float* c_hat, const float* m_hat,
-                      const float* budget, float pi_min, int32_t design, float* pi,
-                      double* objective, int32_t* iters, int32_t* d_status, void* stream) {
+int pair_design_alloc_ex(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                         const float* p_hat, const float* c_hat, const float* m_hat,
+                         const float* budget, float pi_min, int32_t design, const float* pi_prev,
+                         int32_t max_sweeps, float* pi, double* objective, int32_t* iters,
+                         double* residual, int32_t* d_status, void* stream) {
   if (offsets == nullptr || p_hat == nullptr || c_hat == nullptr || budget == nullptr ||
       pi == nullptr)
     return PAIR_EINVAL;
@@ -201,8 +202,18 @@ int pair_design_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offset
   if (gmax < 1 || gmax > PAIR_GMAX_LIMIT) return PAIR_ERANGE;
   if (design < PAIR_DESIGN_PAIR || design > PAIR_DESIGN_UNIFORM) return PAIR_EINVAL;
   if (!(pi_min > 0.0f && pi_min <= 1.0f)) return PAIR_ERANGE;
-  return pair::launch_alloc(B, nv, gmax, offsets, p_hat, c_hat, m_hat, budget, pi_min, design, pi,
-                            objective, iters, d_status, as_stream(stream));
+  if (max_sweeps < 0) return PAIR_ERANGE;
+  return pair::launch_alloc(B, nv, gmax, offsets, p_hat, c_hat, m_hat, budget, pi_min, design,
+                            pi_prev, max_sweeps, pi, objective, iters, residual, d_status,
+                            as_stream(stream));
+}
+
+int pair_design_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,
+                      const float* p_hat, const float* c_hat, const float* m_hat,
+                      const float* budget, float pi_min, int32_t design, float* pi,
+                      double* objective, int32_t* iters, int32_t* d_status, void* stream) {
+  return pair_design_alloc_ex(B, nv, gmax, offsets, p_hat, c_hat, m_hat, budget, pi_min, design,
+                              nullptr, 0, pi, objective, iters, nullptr, d_status, stream);
 }
 
 int pair_cps_fit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,

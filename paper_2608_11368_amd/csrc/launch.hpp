@@ -48,9 +48,11 @@ int launch_audit_noalloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* off
                          double* bias_norm, float* rep_sqerr, int32_t* edge_count,
                          int32_t* d_status, hipStream_t stream);
 
+// max_sweeps <= 0: the library's default cap on a prompt's coordinate sweeps.
 int launch_alloc(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, const float* p_hat,
                  const float* c_hat, const float* m_hat, const float* budget, float pi_min,
-                 int32_t design, float* pi, double* objective, int32_t* iters, int32_t* d_status,
+                 int32_t design, const float* pi_prev, int32_t max_sweeps, float* pi,
+                 double* objective, int32_t* iters, double* residual, int32_t* d_status,
                  hipStream_t stream);
 
 int launch_cps_fit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets,

@@ -141,6 +141,22 @@ def test_audit_noalloc_rejects_bad_arguments_and_oversized_prompts():
     assert "scratch" in pair.strerror(-7)
 
 
+def test_design_alloc_ex_rejects_bad_arguments():
+    f = pair.lib().pair_design_alloc_ex
+
+    def call(B=4, gmax=8, off=FAKE, pi=FAKE, design=0, pi_min=0.08, max_sweeps=0):
+        return f(B, 32, gmax, off, FAKE, FAKE, NULL, FAKE, pi_min, design, NULL, max_sweeps, pi,
+                 NULL, NULL, NULL, NULL, NULL)
+
+    assert call(off=NULL) == -1
+    assert call(pi=NULL) == -1
+    assert call(B=0) == -1
+    assert call(gmax=65) == -3
+    assert call(design=3) == -1
+    assert call(pi_min=0.0) == -3
+    assert call(max_sweeps=-1) == -3
+
+
 def test_binding_checks_tensors_before_calling():
     import torch
 

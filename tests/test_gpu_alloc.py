@@ -139,3 +139,106 @@ def test_full_ragged_batch_sampled_against_oracle():
         rel = (got["objective"][b] - want["objective"]) / want["objective"]
         assert rel <= 1e-6 and abs(rel) <= 1e-6, (b, rel)
     log(f"  sweeps: mean {got['iters'].mean():.1f}, max {got['iters'].max()}")
+
+
+def _run_ex(offsets, inp, design, gmax, pi_prev=None, max_sweeps=0, pi_min=PI_MIN):
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    out = pair.design_alloc(t(offsets), t(inp.p_hat), t(inp.c_hat), t(inp.budget), gmax,
+                            pi_min=pi_min, design=design,
+                            pi_prev=None if pi_prev is None else t(pi_prev),
+                            max_sweeps=max_sweeps)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+@pytest.mark.parametrize("design", [pair.DESIGN_PAIR, pair.DESIGN_POINTWISE, pair.DESIGN_UNIFORM])
+def test_solver_residual_against_oracle_kkt(design):
+    """The residual the solver logs (App. C) is the KKT residual of the
+    design's program at the returned fp32 probabilities: the oracle's
+    checker on the same probabilities gives the same value."""
+    w = wl.WORKLOADS["ragged"].replace(B=40)
+    meta = wl.host_meta(w)
+    inp = wl.alloc_inputs(w, meta.offsets)
+    log(f"solver residual, design {design}")
+    got = _run_ex(meta.offsets, inp, design, meta.gmax)
+    assert got["status"][0] == 0 and np.all(got["iters"] >= 0)
+    pmin = float(np.float32(PI_MIN))
+    worst = 0.0
+    for b in range(meta.B):
+        lo, hi = meta.offsets[b], meta.offsets[b + 1]
+        pg = got["pi"][lo:hi].astype(np.float64)
+        pv = inp.p_hat[lo:hi].astype(np.float64)
+        c = inp.c_hat[lo:hi].astype(np.float64)
+        a = alloc.edge_proxy(pv)
+        if design == pair.DESIGN_POINTWISE:
+            want = alloc.kkt_residual(pg, np.zeros_like(a), pv * (1 - pv), c, float(inp.budget[b]),
+                                      pmin)[0]
+        else:
+            want = alloc.kkt_residual(pg, a, alloc.vertex_term(a), c, float(inp.budget[b]), pmin)[0]
+        r = got["residual"][b]
+        worst = max(worst, abs(r - want) / max(want, 1e-12))
+        assert abs(r - want) <= 1e-9 + 1e-6 * want, (b, r, want)
+        if design != pair.DESIGN_UNIFORM:
+            assert r <= 1e-5
+    if design == pair.DESIGN_UNIFORM:      # one probability is not the PAIR optimum
+        assert got["residual"].max() > 1e-3
+    log(f"  residual vs oracle checker: worst relative difference {worst:.2e}, "
+        f"largest residual {got['residual'].max():.2e}")
+
+
+@pytest.mark.parametrize("design", [pair.DESIGN_PAIR, pair.DESIGN_POINTWISE])
+def test_solver_failure_falls_back_to_uniform(design):
+    """A sweep cap the solver cannot converge within: every prompt whose
+    budget binds falls back to the uniform design of the same expected cost
+    (App. C), with the status bit, negative sweep counts, and probabilities
+    equal to the oracle's uniform design up to fp32 rounding."""
+    w = wl.WORKLOADS["ragged"].replace(B=32)
+    meta = wl.host_meta(w)
+    inp = wl.alloc_inputs(w, meta.offsets)
+    log(f"forced solver failure, design {design}")
+    got = _run_ex(meta.offsets, inp, design, meta.gmax, max_sweeps=2)
+    assert got["status"][0] & pair.ST_SOLVER
+    assert np.all(got["iters"] < 0) and np.all(got["iters"] >= -2)
+    want = alloc.solve_batch(meta.offsets, inp.p_hat.astype(np.float64),
+                             inp.c_hat.astype(np.float64), inp.budget.astype(np.float64), PI_MIN,
+                             design=alloc.UNIFORM)
+    assert np.allclose(got["pi"], want["pi"], rtol=2e-7, atol=0)
+    for b in range(meta.B):
+        lo, hi = meta.offsets[b], meta.offsets[b + 1]
+        spent = inp.c_hat[lo:hi].astype(np.float64) @ got["pi"][lo:hi].astype(np.float64)
+        assert abs(spent / float(inp.budget[b]) - 1.0) <= 1e-6
+    # the same inputs with the default cap converge, with no status bit
+    ok = _run_ex(meta.offsets, inp, design, meta.gmax)
+    assert ok["status"][0] == 0 and np.all(ok["iters"] > 2)
+
+
+def test_solver_warm_start():
+    """Warm starts from the previous step's probabilities (App. C): from the
+    optimum itself the solver needs a fraction of the cold sweeps and returns
+    the same design; from a perturbed start, from one probability for all and
+    from a start with NaN and out-of-range entries it reaches the same
+    optimum (the program is strictly convex)."""
+    w = wl.WORKLOADS["ragged"].replace(B=64)
+    meta = wl.host_meta(w)
+    inp = wl.alloc_inputs(w, meta.offsets)
+    cold = _run_ex(meta.offsets, inp, pair.DESIGN_PAIR, meta.gmax)
+    assert cold["status"][0] == 0
+    rng = np.random.default_rng(11)
+    starts = {
+        "optimum": cold["pi"],
+        "perturbed": np.clip(cold["pi"] * rng.uniform(0.7, 1.3, meta.nv), 0.0, 1.0).astype(np.float32),
+        "uniform": np.full(meta.nv, 0.5, dtype=np.float32),
+        "nan": np.where(rng.random(meta.nv) < 0.2, np.nan,
+                        rng.uniform(-0.5, 1.5, meta.nv)).astype(np.float32),
+    }
+    for name, start in starts.items():
+        warm = _run_ex(meta.offsets, inp, pair.DESIGN_PAIR, meta.gmax, pi_prev=start)
+        assert warm["status"][0] == 0 and np.all(warm["iters"] >= 0), name
+        rel_obj = np.abs(warm["objective"] / cold["objective"] - 1.0).max()
+        rel_pi = np.abs(warm["pi"].astype(np.float64) / cold["pi"] - 1.0).max()
+        log(f"  warm start {name}: sweeps mean {warm['iters'].mean():.1f} "
+            f"(cold {cold['iters'].mean():.1f}), max |obj rel| {rel_obj:.1e}, max pi rel {rel_pi:.1e}")
+        assert rel_obj <= 1e-9 and rel_pi <= 1e-4, name
+        assert warm["residual"].max() <= 1e-5
+        if name == "optimum":
+            assert warm["iters"].mean() <= 0.5 * cold["iters"].mean()
