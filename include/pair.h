@@ -373,10 +373,14 @@ size_t pair_audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R)
  *     bias = || (1/R) sum_r g_r - t ||
  * The R x D estimates are never materialised: (A~^(r) - a) times S_b runs on
  * the matrix cores with the squared norm reduced in the epilogue.  Operands
- * are fp16 after exact power-of-two rescaling (score rows by their largest
- * magnitude, which makes the bf16 -> fp16 conversion exact; each replicate
- * row of A~^(r) - a by its largest entry, then one fp16 rounding), so e_r
- * carries a relative error of about 2^-11 per coefficient.  The bias row
+ * are fp16 after power-of-two rescaling: each score row by its largest
+ * magnitude within a column slice, then rounded to nearest fp16, which is
+ * exact for entries within 2^17 of that maximum and off by at most 2^-25 of
+ * it below; each replicate row of A~^(r) - a by its largest entry, then one
+ * fp16 rounding (2^-11 relative).  With y_r = (A~^(r) - a) S_b and u = 2^-11,
+ * |Delta e_r| <= 2 |y_r| (u || |A~^(r) - a| |S_b| || + 2^-25 sum_i
+ * |A~^(r)_i - a_i| M_i sqrt(D)) to first order, M_i row i's largest
+ * magnitude: about u relative unless the deviations cancel.  The bias row
  * (1/R) sum_r (A~^(r) - a) is applied in fp32 on the vector units, without
  * that rounding.  A replicate's e_r does not depend on R or rep0: calls over
  * consecutive replicate ranges return bitwise the rep_sqerr of one call over

@@ -27,12 +27,15 @@
 //  3. audit_mfma    the contraction on v_mfma_f32_32x32x16_f16.  Each score
 //                   row of a column slice is rescaled by 2^-e_i, with e_i
 //                   the exponent of the row's largest magnitude within the
-//                   slice, which makes the bf16 -> fp16 conversion exact
-//                   (8 significant bits fit in 11); each
+//                   slice, and rounded to fp16 (to nearest), which is exact
+//                   for every entry within 2^17 of that maximum and off by
+//                   at most 2^-25 of it below (8 significant bits fit in
+//                   11, down to fp16's subnormals); each
 //                   replicate row of delta is rescaled by 2^(e_i - f_r), with
 //                   f_r chosen so its largest entry lies in [1, 2), and rounded
-//                   once to fp16 (2^-11 relative).  The products are exact
-//                   rescalings of delta_r S_b, so e_r = 4^f_r * sum of squares.
+//                   once to fp16 (2^-11 relative).  The products are
+//                   rescalings of delta_r S_b by 2^-f_r, so e_r = 4^f_r * sum
+//                   of squares.
 //                   A workgroup owns one prompt and one slice of score
 //                   columns: the slice is converted once into LDS and every
 //                   replicate row sweeps over it, so S_b is read from HBM
@@ -433,8 +436,11 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
   // columns past D and rows past G read as zero) and finds each row's largest
   // magnitude within the slice as bf16 bits (integer order = magnitude
   // order).  Pass 2 rescales row i by 2^-e_i, 2^e_i <= max |s_i| < 2^(e_i+1),
-  // and converts to fp16 (exact for every value within 2^17 of that
-  // maximum).
+  // and converts to fp16 with round-to-nearest-even: exact for every value
+  // within 2^17 of that maximum (8 significant bits fit in fp16's normal
+  // range and its subnormals down to 2^-17); smaller values land on fp16's
+  // subnormal grid of 2^-24, an absolute error of at most 2^-25 of the row's
+  // slice maximum.
   uint4 pv[kPerThread];
   {
     const uint16_t* sb = scores + o0 * ld;
@@ -518,9 +524,8 @@ __global__ __launch_bounds__(kMfmaThreads) __attribute__((amdgpu_waves_per_eu(KS
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         const float lo = ldexpf(bf16lo_to_f32(w4[k]), ne), hi = ldexpf(bf16hi_to_f32(w4[k]), ne);
-        const uint32_t hpair = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(lo, hi));
-        dst[(2 * k) * KP] = (uint16_t)hpair;
-        dst[(2 * k + 1) * KP] = (uint16_t)(hpair >> 16);
+        dst[(2 * k) * KP] = __builtin_bit_cast(uint16_t, (_Float16)lo);
+        dst[(2 * k + 1) * KP] = __builtin_bit_cast(uint16_t, (_Float16)hi);
       }
     }
   }

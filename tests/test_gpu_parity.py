@@ -499,6 +499,19 @@ def _audit_case(w, meta, R, rep0=0, pi_w=None, want_reps=True):
     return got, want
 
 
+def _wide_range_scores(kind, nv, D, seed):
+    """Score rows of wide dynamic range as bf16 bits: magnitudes log-uniform
+    over 2^-30 .. 2^0 with random signs, or standard Cauchy entries (heavy
+    tails: a row's largest entry is hundreds of times its typical one)."""
+    rng = np.random.default_rng(seed)
+    if kind == "loguniform":
+        x = np.exp2(-30.0 * rng.random((nv, D))) * np.where(rng.random((nv, D)) < 0.5, -1.0, 1.0)
+    else:
+        x = np.tan(np.pi * (rng.random((nv, D)) - 0.5))
+    return torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).view(torch.int16) \
+        .numpy().view(np.uint16)
+
+
 def _check_audit(got, want, label):
     mse, bias = got["mse"].cpu().numpy(), got["bias_norm"].cpu().numpy()
     assert int(got["status"].item()) == 0
@@ -524,6 +537,26 @@ def test_audit_reduced_vs_oracle(name, B, D, R, G):
     log(f"audit {name} B={B} D={D} R={R} gmax={meta.gmax}")
     got, want = _audit_case(w, meta, R)
     _check_audit(got, want, name)
+
+
+@pytest.mark.parametrize("kind", ["loguniform", "cauchy"])
+@pytest.mark.parametrize("G", [16, 64])
+def test_audit_wide_dynamic_range(kind, G):
+    """Score rows whose entries span many binades: the matrix-core operands
+    are the rows rescaled by their slice maximum and rounded to fp16, exact
+    within 2^17 of that maximum and rounded to nearest below; the audit must
+    still match the oracle within the audit's bars."""
+    w = wl.WORKLOADS["audit"].replace(B=4, D=3000, G=G, dtype=wl.BF16)
+    meta = wl.host_meta(w)
+    s = _wide_range_scores(kind, meta.nv, w.D, 900 + G)
+    log(f"audit wide range {kind} G={G} B={meta.B} D={w.D}")
+    dm = upload_meta(meta)
+    R = 300
+    got = pair.audit(dm["offsets"], scores_to_device(s, w), dm["rewards"], dm["p"], w.design_seed,
+                     0, R, meta.gmax, nv=meta.nv)
+    torch.cuda.synchronize()
+    want = oracle.audit(meta.offsets, s, meta.rewards, meta.p, w.design_seed, 0, R)
+    _check_audit(got, want, f"{kind} G={G}")
 
 
 def test_audit_unweighted_and_resumable():
