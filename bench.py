@@ -15,13 +15,16 @@ Prints ONE JSON line.  `value` is the gradient chain's throughput in GB/s of
 algorithmic bytes (score rows with a nonzero coefficient, the coefficients,
 and the fp32 output), i.e. bytes that must cross HBM, over the chain's event
 time.  The audit is reported in replicate-estimates/s and TFLOP/s (2*G*D flop
-per replicate estimate) in the "audit" object.  "roofline" is for the
-weighted-gradient kernel (the kernel `value` measures), timed with HIP events
-on the stream it is launched on.
+per replicate estimate of the prompts it sweeps) in the "audit" object.
+"roofline" is the weighted-gradient kernel on the worst of the three gradient
+workloads (b128, the Qwen3-shaped slice, ragged), each timed with HIP events on
+the stream it is launched on; "roofline_by_config" lists all of them, per
+prompt and in batch-mean mode.
 
 Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--no-cpu-baseline]
        python bench.py --copy-calibration     (1 GiB copy for counter scaling)
        python bench.py --audit-calls N        (N audit calls only, for counter passes)
+       python bench.py --counter-pass         (the calls the traffic counter runs profile)
        python bench.py --record-traffic DIR   (counter runs -> profiles/counters.json)
 """
 from __future__ import annotations
@@ -81,19 +84,21 @@ def _traffic(kernel, sources):
     return rec.get("hbm_bytes_per_launch")
 
 
-# Kernels whose HBM traffic is recorded from rocprofv3 counter runs of this
-# script: key -> (kernel-name prefix of every dispatch the entry point makes,
-# name of the dispatch counted once per call, sources the record is tied to).
-TRAFFIC_KERNELS = {
-    "wgrad_b128": ("wgrad_kernel", "wgrad_kernel", ["wgrad.hip", "common.hpp"]),
-    "audit_b256": ("audit_", "audit_final_kernel", ["audit.hip", "common.hpp"]),
-}
-
-
-# The counter runs use `--steps 2 --warmup 1`: the first three calls of each
-# traffic kernel in dispatch order are the main loop's.
-COUNTER_RUN_STEPS = 2
-COUNTER_RUN_WARMUP = 1
+# Kernels whose HBM traffic is recorded from rocprofv3 counter runs of
+# `bench.py --counter-pass`, which makes COUNTER_PASS_CALLS calls of each entry
+# point below in this order: per-prompt and batch-mean weighted gradient on
+# each workload of GRAD_WORKLOADS, then the audit.  Key -> (kernel-name prefix
+# of every dispatch of one call, the dispatch counted once per call, index of
+# the call group of that name in pass order, sources the record is tied to).
+GRAD_WORKLOADS = ("b128", "qwen3", "ragged")
+COUNTER_PASS_CALLS = 2
+TRAFFIC_KERNELS = {}
+for _k, _name in enumerate(GRAD_WORKLOADS):
+    TRAFFIC_KERNELS[f"wgrad_{_name}"] = ("wgrad_kernel", "wgrad_kernel", _k,
+                                         ["wgrad.hip", "common.hpp"])
+    TRAFFIC_KERNELS[f"wgrad_mean_{_name}"] = ("wgrad_mean_kernel", "wgrad_mean_kernel", _k,
+                                              ["wgrad.hip", "common.hpp"])
+TRAFFIC_KERNELS["audit_b256"] = ("audit_", "audit_final_kernel", 0, ["audit.hip", "common.hpp"])
 
 
 def _counter_rows(path):
@@ -102,33 +107,34 @@ def _counter_rows(path):
         return [(r["Kernel_Name"], float(r["Counter_Value"])) for r in csv.DictReader(f)]
 
 
-def _kernel_kib(rows, prefix, per_call, calls):
-    """KiB per entry-point call over the first `calls` calls in dispatch order
-    (the main timed loop of the counter run; later dispatches of the same
-    kernels belong to other workloads): all dispatches whose demangled name
-    starts with `prefix` (namespaces dropped), up to and including the
-    `calls`-th dispatch named `per_call`, over `calls`."""
+def _kernel_kib(rows, prefix, per_call, group, calls):
+    """KiB per entry-point call for call group `group` of the counter pass:
+    the dispatches whose demangled name starts with `prefix` (namespaces
+    dropped) from the one after the (group * calls)-th dispatch named
+    `per_call` up to and including the ((group + 1) * calls)-th, over
+    `calls`."""
     def base(name):
         name = name.replace("(anonymous namespace)::", "")
         name = name[5:] if name.startswith("void ") else name
         return name.split("(")[0].split("<")[0].split("::")[-1].strip()
     tot, seen = 0.0, 0
+    lo, hi = group * calls, (group + 1) * calls
     for n, v in rows:
         b = base(n)
-        if b.startswith(prefix):
+        if b.startswith(prefix) and lo <= seen < hi:
             tot += v
         if b == per_call:
             seen += 1
-            if seen == calls:
+            if seen == hi:
                 return tot / calls
-    raise SystemExit(f"fewer than {calls} {per_call} dispatches in the counter file")
+    raise SystemExit(f"fewer than {hi} {per_call} dispatches in the counter file")
 
 
 def record_traffic(folder):
     """Write HBM bytes per launch into the committed counter record from four
     rocprofv3 --pmc runs under `folder`: tr_FETCH_SIZE/, tr_WRITE_SIZE/ (this
-    script with --no-cpu-baseline --steps 2 --warmup 1) and trc_FETCH_SIZE/,
-    trc_WRITE_SIZE/ (this script with --copy-calibration).  Each counter is
+    script with --counter-pass) and trc_FETCH_SIZE/, trc_WRITE_SIZE/ (this
+    script with --copy-calibration).  Each counter is
     scaled by the factor that maps it to the known bytes of the calibration
     copy (1 GiB read, 1 GiB written)."""
     def rows(sub):
@@ -149,10 +155,10 @@ def record_traffic(folder):
         rec = {}
     fetch_rows, write_rows = rows("tr_FETCH_SIZE"), rows("tr_WRITE_SIZE")
     cmd = "rocprofv3 --pmc {c} -f csv -d <out> -o run -- python -u <repo>/bench.py {a}"
-    calls = COUNTER_RUN_STEPS + COUNTER_RUN_WARMUP      # main-loop calls of the counter run
-    for key, (prefix, per_call, sources) in TRAFFIC_KERNELS.items():
-        fk = _kernel_kib(fetch_rows, prefix, per_call, calls)
-        wk = _kernel_kib(write_rows, prefix, per_call, calls)
+    calls = COUNTER_PASS_CALLS
+    for key, (prefix, per_call, group, sources) in TRAFFIC_KERNELS.items():
+        fk = _kernel_kib(fetch_rows, prefix, per_call, group, calls)
+        wk = _kernel_kib(write_rows, prefix, per_call, group, calls)
         rd, wr = fk * 1024.0 * fetch_f, wk * 1024.0 * write_f
         rec[key] = {
             "kernels": prefix + "*",
@@ -166,10 +172,8 @@ def record_traffic(folder):
             "hbm_read_bytes_per_launch": int(rd),
             "hbm_write_bytes_per_launch": int(wr),
             "hbm_bytes_per_launch": int(rd + wr),
-            "main_loop_calls_counted": calls,
-            "commands": [cmd.format(c=c, a=a) for a in
-                         (f"--no-cpu-baseline --steps {COUNTER_RUN_STEPS} --warmup "
-                          f"{COUNTER_RUN_WARMUP}", "--copy-calibration")
+            "calls_counted": calls,
+            "commands": [cmd.format(c=c, a=a) for a in ("--counter-pass", "--copy-calibration")
                          for c in ("FETCH_SIZE", "WRITE_SIZE")],
         }
     with open(COUNTERS, "w") as f:
@@ -419,7 +423,8 @@ def time_wgrad_configs(pair, stream, wl, dev, coeff, out, scores, off, rew, p, m
                                                                 status, stream), 10)
         alg = nz * D * 2 + nv * 4 + (B + 1) * 8 + D * 4
         res["b128_batch_mean"] = {"ms": round(ms, 4), "GBps": round(alg / ms / 1e6, 1),
-                                  "frac": round(alg / ms / 1e6 / HBM_PEAK_GBPS, 4)}
+                                  "frac": round(alg / ms / 1e6 / HBM_PEAK_GBPS, 4),
+                                  "algorithmic_bytes": alg}
     del mean
     for name in ("qwen3", "ragged"):
         wk = wl.WORKLOADS[name]
@@ -447,11 +452,12 @@ def time_wgrad_configs(pair, stream, wl, dev, coeff, out, scores, off, rew, p, m
         res[name] = {"B": meta.B, "nv": meta.nv, "D": wk.D, "rows_nonzero": nz,
                      "ms": round(ms, 4), "GBps": round(alg / ms / 1e6, 1),
                      "score_only_GBps": round(nz * wk.D * 2 / ms / 1e6, 1),
-                     "frac": round(alg / ms / 1e6 / HBM_PEAK_GBPS, 4)}
+                     "frac": round(alg / ms / 1e6 / HBM_PEAK_GBPS, 4), "algorithmic_bytes": alg}
         alg_mean = nz * wk.D * 2 + meta.nv * 4 + (meta.B + 1) * 8 + wk.D * 4
         res[name + "_batch_mean"] = {"ms": round(ms_mean, 4),
                                      "GBps": round(alg_mean / ms_mean / 1e6, 1),
-                                     "frac": round(alg_mean / ms_mean / 1e6 / HBM_PEAK_GBPS, 4)}
+                                     "frac": round(alg_mean / ms_mean / 1e6 / HBM_PEAK_GBPS, 4),
+                                     "algorithmic_bytes": alg_mean}
         del s_k, mean_k
         torch.cuda.empty_cache()
     if int(status.item()) != 0:
@@ -742,6 +748,42 @@ def copy_calibration(gib=1.0, reps=5):
                       "read_GBps": round(4 * n * 2 / (read_ms * 1e-3) / 1e9, 1)}), flush=True)
 
 
+def counter_pass():
+    """The program the traffic counter runs profile: COUNTER_PASS_CALLS calls
+    each of the per-prompt and the batch-mean weighted gradient on every
+    workload of GRAD_WORKLOADS, then of the audit on the audit workload, each
+    call followed by a synchronisation, in that order."""
+    import torch
+
+    import paper_2608_11368_amd as pair
+    import workloads as wl
+
+    dev = torch.device("cuda:0")
+    st = torch.zeros(1, dtype=torch.int32, device=dev)
+    for name in GRAD_WORKLOADS:
+        w = wl.WORKLOADS[name]
+        m = wl.host_meta(w)
+        off, rew, p = (torch.from_numpy(a).to(dev) for a in (m.offsets, m.rewards, m.p))
+        s = wl.device_scores(w, m.nv, dev)
+        coeff = torch.empty(m.nv, dtype=torch.float32, device=dev)
+        pair.pair_design_coeffs(m.B, m.nv, m.gmax, off, p, rew, w.design_seed, 0, coeff, None,
+                                None, None, None, st)
+        out = torch.empty((m.B, w.D), dtype=torch.float32, device=dev)
+        mean = torch.empty(w.D, dtype=torch.float32, device=dev)
+        torch.cuda.synchronize()
+        for reduce, o in ((0, out), (1, mean)):
+            for _ in range(COUNTER_PASS_CALLS):
+                pair.pair_weighted_grad(m.B, m.nv, off, s, coeff, o, reduce, st)
+                torch.cuda.synchronize()
+        print(json.dumps({"counter_pass": name, "nonzero_rows": int(torch.count_nonzero(coeff))}),
+              flush=True)
+        del s, out, mean
+        torch.cuda.empty_cache()
+    audit_calls(COUNTER_PASS_CALLS)
+    if int(st.item()) != 0:
+        raise RuntimeError(f"device status {int(st.item())} in the counter pass")
+
+
 def audit_calls(n):
     """`n` plain pair_audit calls on the audit workload (B=256, G=16,
     D=65536, R=4096), each followed by a synchronisation, and nothing else:
@@ -778,6 +820,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--audit-calls", type=int, default=0, metavar="N")
+    ap.add_argument("--counter-pass", action="store_true",
+                    help="the fixed sequence of calls the traffic counter runs profile")
     ap.add_argument("--record-traffic", metavar="DIR",
                     help="write profiles/counters.json from rocprofv3 --pmc runs under DIR")
     args = ap.parse_args()
@@ -802,6 +846,9 @@ def main():
         return
     if args.audit_calls > 0:
         audit_calls(args.audit_calls)
+        return
+    if args.counter_pass:
+        counter_pass()
         return
 
     dev = torch.device("cuda:0")
@@ -893,11 +940,16 @@ def main():
     flops_audit = 2.0 * live_a * R * Ga * Da
     tflops_audit = flops_audit / (ms_audit * 1e-3) / 1e12
 
-    roof_w = {"kernel": "wgrad_kernel<bf16> (pair_weighted_grad)", "bound": "hbm",
-              "achieved": round(gbps_wgrad, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-              "frac": round(gbps_wgrad / HBM_PEAK_GBPS, 4),
-              "traffic": _traffic("wgrad_b128", ["wgrad.hip", "common.hpp"]),
-              "ms": round(ms_wgrad, 4), "algorithmic_bytes": bytes_wgrad}
+    def roof_wgrad(key, kernel, ms, alg):
+        gbps = alg / (ms * 1e-3) / 1e9
+        return {"kernel": kernel, "workload": key.split("_")[-1], "bound": "hbm",
+                "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                "traffic": _traffic(key, ["wgrad.hip", "common.hpp"]),
+                "ms": round(ms, 4), "algorithmic_bytes": alg}
+
+    roof_w = roof_wgrad("wgrad_b128", "wgrad_kernel<bf16> (pair_weighted_grad)", ms_wgrad,
+                        bytes_wgrad)
     roof_a = {"kernel": "pair_audit (coeffs + mean + mfma + finalize)", "bound": "mfma",
               "achieved": round(tflops_audit, 1), "peak": BF16_MFMA_PEAK_TFLOPS,
               "unit": "TFLOP/s", "frac": round(tflops_audit / BF16_MFMA_PEAK_TFLOPS, 4),
@@ -923,7 +975,8 @@ def main():
         "score_dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": "b128 gradient chain + audit",
+            "workload": "b128 gradient chain + audit (timed step); per-prompt and batch-mean "
+                        "gradient on b128, qwen3 and ragged",
             "grad": {"B": B, "G": G, "D": D, "scores": "bf16 N(0,1/D)", "nv": nv,
                      "rows_nonzero": nz_rows},
             "audit": {"B": Ba, "G": Ga, "D": Da, "R": R, "scores": "bf16 N(0,1/D)"},
@@ -936,9 +989,28 @@ def main():
         "audit": {"value": round(Ba * R / (ms_audit * 1e-3), 1),
                   "unit": "replicate-estimates/s", "roofline": roof_a},
     }
-    result["wgrad_configs"] = time_wgrad_configs(pair, stream, wl, dev, coeff, out, scores, off,
-                                                 rew, p, mask, pi, ec, comp, status, B, nv, G, D,
-                                                 w)
+    cfgs = time_wgrad_configs(pair, stream, wl, dev, coeff, out, scores, off, rew, p, mask, pi,
+                              ec, comp, status, B, nv, G, D, w)
+    result["wgrad_configs"] = cfgs
+    # The headline roofline is the worst per-prompt weighted gradient of the
+    # three gradient workloads in this run; every one, and the batch-mean
+    # mode of each, is listed beside it.
+    by_cfg = {"b128": roof_w}
+    for name in ("qwen3", "ragged"):
+        by_cfg[name] = roof_wgrad(f"wgrad_{name}", "wgrad_kernel<bf16> (pair_weighted_grad)",
+                                  cfgs[name]["ms"], cfgs[name]["algorithmic_bytes"])
+    for name in GRAD_WORKLOADS:
+        rec = cfgs[name + "_batch_mean"]
+        by_cfg[name + "_batch_mean"] = roof_wgrad(
+            f"wgrad_mean_{name}", "wgrad_mean_kernel<bf16> (pair_weighted_grad, reduce=1)",
+            rec["ms"], rec["algorithmic_bytes"])
+    worst = min(GRAD_WORKLOADS, key=lambda k: by_cfg[k]["frac"])
+    result["roofline"] = dict(by_cfg[worst], selection="worst per-prompt weighted gradient of "
+                              "the b128, qwen3 and ragged workloads in this run")
+    result["roofline_by_config"] = by_cfg
+    result["config"]["grad_configs"] = {
+        name: {k: cfgs[name][k] for k in ("B", "nv", "D", "rows_nonzero")}
+        for name in ("qwen3", "ragged")}
     result["exact_audit"] = time_exact_audit(pair, stream, Ba, nva, Ga, off_a, scores_a, rew_a,
                                              p_a, Da)
     result["design_alloc"] = time_alloc(pair, stream, wl, dev)
