@@ -72,21 +72,34 @@ struct PieceTraits<false> {
 // TAIL = false: every tile of the launch lies wholly inside [0, D).
 // TAIL = true: the launch holds the last tile of each prompt, which may end
 // inside a piece; columns past D are neither read nor written.
-// Workgroup x of the launch covers prompt x / tiles_per_prompt and tile
-// tile0 + x % tiles_per_prompt.
+// Workgroup order of the full-tile launch: groups of `ilv` consecutive
+// prompts (fewer in the last group), and within a group consecutive
+// workgroups take the group's prompts in turn at the same tile, so that ilv
+// prompts' rows stream at once (hardware deals consecutive workgroups to the
+// 8 XCDs in turn; 1, 2 or 4 keeps a prompt on a fixed set of XCDs).  The tail
+// launch covers prompt x with workgroup x.
 template <bool BF16, bool TAIL>
 __global__ __launch_bounds__(kThreads) void wgrad_kernel(
     int64_t B, int64_t nv, const int64_t* __restrict__ offsets,
     const unsigned char* __restrict__ scores, int64_t row_bytes, const float* __restrict__ coeff,
-    float* __restrict__ out, int64_t D, int64_t tiles_per_prompt, int64_t tile0, int vec_out,
-    int32_t* d_status) {
+    float* __restrict__ out, int64_t D, int64_t tiles_per_prompt, int64_t tile0, int64_t ilv,
+    int vec_out, int32_t* d_status) {
   using T = PieceTraits<BF16>;
   constexpr int NP = T::kPieces;
   constexpr int64_t kSpan = (int64_t)kThreads * kPieceCols;   // columns per piece index
   constexpr int64_t kTileCols = kSpan * NP;
 
-  const int64_t b = blockIdx.x / tiles_per_prompt;
-  const int64_t tile = tile0 + (blockIdx.x - b * tiles_per_prompt);
+  int64_t b, tile;
+  if (TAIL) {
+    b = blockIdx.x / tiles_per_prompt;
+    tile = tile0 + (blockIdx.x - b * tiles_per_prompt);
+  } else {
+    const int64_t grp = blockIdx.x / (ilv * tiles_per_prompt);
+    const int64_t r = blockIdx.x - grp * ilv * tiles_per_prompt;
+    const int64_t k = B - ilv * grp < ilv ? B - ilv * grp : ilv;   // prompts in this group
+    b = ilv * grp + r % k;
+    tile = tile0 + r / k;
+  }
   if (b >= B) return;
   const int lane = threadIdx.x & (kWave - 1);
   int64_t o0, g;
@@ -340,9 +353,14 @@ int launch_wgrad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D, const
   const int64_t full_tiles = D / tile;                 // tiles wholly inside [0, D)
   const bool tail = full_tiles * tile < D;
   if (B * full_tiles > 0x7fffffffLL) return PAIR_ERANGE;
+  // Prompts streamed at once (see wgrad_kernel): 4 for groups of at most 8
+  // rollouts on average, else 2.  Measured on b128 (G = 16), the Qwen3-shaped
+  // slice (G = 8) and ragged (mean G 33), against one prompt at a time: +1.5,
+  // +2.4 and +0.7 points of HBM peak; 3, 6, 8 and 16 were slower.
+  const int64_t ilv = nv <= 8 * B ? 4 : 2;
 #define PAIR_WGRAD(BF, TL, GRID, TPP, T0)                                                         \
   hipLaunchKernelGGL((wgrad_kernel<BF, TL>), dim3((unsigned)(GRID)), dim3(kThreads), 0, stream, B, \
-                     nv, offsets, s, row_bytes, coeff, out, D, TPP, T0, vec_out, d_status)
+                     nv, offsets, s, row_bytes, coeff, out, D, TPP, T0, ilv, vec_out, d_status)
   if (full_tiles > 0) {
     if (bf16) {
       PAIR_WGRAD(true, false, B * full_tiles, full_tiles, 0);
