@@ -636,6 +636,16 @@ def test_audit_equal_reward_prompts():
     sub["status"] = got["status"]
     want_live = {k: want[k][live] for k in ("mse", "bias_norm", "rep_sqerr", "edge_count")}
     _check_audit(sub, want_live, "live prompts")
+    # every prompt with equal rewards: nothing is swept, everything is exactly zero
+    flat = meta.rewards.copy()
+    flat[:] = 0.5
+    allz = pair.audit(dm["offsets"], scores_to_device(s_nan, w), torch.from_numpy(flat).to(DEV),
+                      dm["p"], w.design_seed, 3, R, meta.gmax, nv=meta.nv)
+    torch.cuda.synchronize()
+    assert int(allz["status"].item()) == 0
+    for name in ("mse", "bias_norm", "rep_sqerr"):
+        assert bool((allz[name] == 0).all()), name
+    assert torch.equal(allz["edge_count"], got["edge_count"])
     # a NaN score in a swept prompt is reported
     b_live = int(np.flatnonzero(live)[0])
     s_bad = s.copy()
