@@ -409,8 +409,9 @@ int pair_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int6
  * memory: code under HIP graph capture, tight serving loops, harnesses that
  * forbid hipMalloc.  The arguments are pair_audit's without the workspace.
  * Its workspace is instead a static device array of the library,
- * PAIR_AUDIT_SCRATCH_BYTES (64 MiB) on each GPU it runs on, held from its
- * first call on that GPU until the process ends.  The prompts are audited in
+ * PAIR_AUDIT_SCRATCH_BYTES (64 MiB), which each GPU the library runs on holds
+ * until the process ends (it is part of the library's device code, whether
+ * or not this entry point is called).  The prompts are audited in
  * consecutive chunks whose pair_audit_workspace_bytes fits that array, so the
  * outputs are bitwise those of pair_audit with the same arguments (the audit
  * workload's shape, G = 16, D = 65536, R = 4096, takes about 80 prompts per
