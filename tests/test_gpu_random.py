@@ -91,7 +91,7 @@ def _case(rng, max_b, widths, bf16=None):
                 host=host[:, :D], dev=dev, seed=seed, rep0=rep0, gmax=int(sizes.max()))
 
 
-@pytest.mark.parametrize("case_id", range(24))
+@pytest.mark.parametrize("case_id", range(96))
 def test_random_gradient_chain(case_id):
     rng = np.random.default_rng(7000 + case_id)
     c = _case(rng, 24, WIDTHS)
@@ -163,7 +163,7 @@ def test_random_gradient_chain(case_id):
     assert err_m <= tol
 
 
-@pytest.mark.parametrize("case_id", range(16))
+@pytest.mark.parametrize("case_id", range(48))
 def test_random_audit(case_id):
     rng = np.random.default_rng(9100 + case_id)
     c = _case(rng, 5, (1, 33, 500, 2047, 2049, 3000), bf16=True)
@@ -202,7 +202,7 @@ def _wmax(rng, rule):
     return float(rng.choice([2.0, 10.0, 50.0])) if rule == pair.RULE_CLIPPED else 0.0
 
 
-@pytest.mark.parametrize("case_id", range(12))
+@pytest.mark.parametrize("case_id", range(36))
 def test_random_rule_coefficients_and_gradient(case_id):
     rng = np.random.default_rng(9500 + case_id)
     c = _case(rng, 16, WIDTHS)
@@ -237,7 +237,7 @@ def test_random_rule_coefficients_and_gradient(case_id):
     assert err <= (BF16_TOL if c["bf16"] else FP32_TOL)
 
 
-@pytest.mark.parametrize("case_id", range(12))
+@pytest.mark.parametrize("case_id", range(24))
 def test_random_rule_audit(case_id):
     rng = np.random.default_rng(9700 + case_id)
     c = _case(rng, 4, (33, 500, 2049), bf16=True)
@@ -276,7 +276,7 @@ def test_random_rule_audit(case_id):
     assert c_err <= 1e-5 and t_err <= 1e-5
 
 
-@pytest.mark.parametrize("case_id", range(8))
+@pytest.mark.parametrize("case_id", range(24))
 def test_random_exact_audit(case_id):
     rng = np.random.default_rng(9900 + case_id)
     c = _case(rng, 6, (1, 100, 513, 2049, 5000), bf16=True)
