@@ -395,8 +395,11 @@ size_t pair_audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R)
  *   edge_count     int32 [B][R] out: observed edges per replicate    (or NULL)
  *   workspace      device scratch of ws_bytes >= pair_audit_workspace_bytes,
  *                  256-byte aligned; contents on entry do not matter
+ * A prompt whose rewards are all equal has A~^(r) - a = 0 in every replicate
+ * (every edge term carries r_i - r_j): its e_r, mse and bias are exact zeros,
+ * its draws and edge counts are still made, and its score rows are not read.
  * Device status: PAIR_ST_BAD_GROUP, PAIR_ST_P_RANGE, PAIR_ST_RHO_RANGE,
- * PAIR_ST_NONFINITE.
+ * PAIR_ST_NONFINITE (a non-finite score of a prompt that is swept).
  */
 int pair_audit(int64_t B, int64_t nv, int32_t gmax, const int64_t* offsets, int64_t D,
                const void* scores, int32_t dtype, int64_t ld, const float* rewards,
