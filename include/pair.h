@@ -377,10 +377,13 @@ size_t pair_audit_workspace_bytes(int64_t B, int32_t gmax, int64_t D, int64_t R)
  * magnitude within a column slice, then rounded to nearest fp16, which is
  * exact for entries within 2^17 of that maximum and off by at most 2^-25 of
  * it below; each replicate row of A~^(r) - a by its largest entry, then one
- * fp16 rounding (2^-11 relative).  With y_r = (A~^(r) - a) S_b and u = 2^-11,
- * |Delta e_r| <= 2 |y_r| (u || |A~^(r) - a| |S_b| || + 2^-25 sum_i
- * |A~^(r)_i - a_i| M_i sqrt(D)) to first order, M_i row i's largest
- * magnitude: about u relative unless the deviations cancel.  The bias row
+ * fp16 rounding (2^-11 relative).  With delta_r = A~^(r) - a, y_r =
+ * delta_r S_b, z_r = S_b y_r^T (so e_r = delta_r . z_r) and u = 2^-11, that
+ * rounding has the same relative error in every score column, so to first
+ * order |Delta e_r| <= 2 u sum_i |delta_ri z_ri|, plus terms of 2^-25 of
+ * the row maxima M_i for fp16 subnormals: at most 2u e_r when the terms
+ * delta_ri z_ri share a sign (near-orthogonal score rows), more only when
+ * they cancel, as with a single score column.  The bias row
  * (1/R) sum_r (A~^(r) - a) is applied in fp32 on the vector units, without
  * that rounding.  A replicate's e_r does not depend on R or rep0: calls over
  * consecutive replicate ranges return bitwise the rep_sqerr of one call over
