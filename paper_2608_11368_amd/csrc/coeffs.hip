@@ -135,7 +135,7 @@ __global__ __launch_bounds__(64) void design_coeffs_kernel(
   if (vert) {
     const Philox4x64 x = philox4x64_10((uint64_t)rep, (uint64_t)b, (uint64_t)(lane >> 2), 0ull,
                                        seed, 0ull);
-    const uint64_t u32 = x.w[lane & 3] >> 32;
+    const uint64_t u32 = philox_word(x, lane & 3) >> 32;
     if (p_in_range(p_i)) {
       J = u32 < inclusion_threshold(p_i) ? 1 : 0;
     } else {

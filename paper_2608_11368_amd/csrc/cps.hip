@@ -71,10 +71,6 @@ __device__ __forceinline__ double pick(const double (&e)[KP], int k) {
   return v;
 }
 
-__device__ __forceinline__ uint64_t philox_word(const Philox4x64& x, int q) {
-  return q == 0 ? x.w[0] : (q == 1 ? x.w[1] : (q == 2 ? x.w[2] : x.w[3]));
-}
-
 // Prefix rows Pf[m][k] = e_k(w_0 .. w_{m-1}), m = 0..g, and suffix rows
 // Sf[m][k] = e_k(w_{m+1} .. w_{g-1}), m = 0..g-1, for k <= n, written to LDS
 // with row stride kS.  Lane k carries coefficient k; adding unit m is

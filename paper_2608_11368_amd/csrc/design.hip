@@ -51,7 +51,7 @@ __global__ __launch_bounds__(256) void design_draw_kernel(
     if (active) {
       const Philox4x64 x = philox4x64_10((uint64_t)(rep0 + r), (uint64_t)b, (uint64_t)(lane >> 2),
                                          0ull, seed, 0ull);
-      const uint64_t u32 = x.w[lane & 3] >> 32;
+      const uint64_t u32 = philox_word(x, lane & 3) >> 32;
       if (p_in_range(pv)) {
         J = u32 < inclusion_threshold(pv) ? 1 : 0;
       } else if (r == 0) {
