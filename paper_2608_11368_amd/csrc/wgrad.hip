@@ -337,14 +337,17 @@ int launch_wgrad(int64_t B, int64_t nv, const int64_t* offsets, int64_t D, const
     // Row groups per workgroup: enough that the grid holds about 8 waves per
     // SIMD of the chip (4 row groups at most, one 1024-thread workgroup).
     const int64_t simds = 4 * (int64_t)device_cu_count();
-    const int rg = grid * 4 >= 8 * simds ? 1 : (grid * 8 >= 8 * simds ? 2 : 4);
+    int rg = grid * 4 >= 8 * simds ? 1 : (grid * 8 >= 8 * simds ? 2 : 4);
+    // fp32 rows take twice the registers per batch: at four row groups (1024
+    // threads, 128 VGPRs a lane) the fp32 kernel would spill, so it stops at two.
+    if (!bf16 && rg > 2) rg = 2;
 #define PAIR_MEAN(BF, RG_)                                                                       \
   hipLaunchKernelGGL((wgrad_mean_kernel<BF, RG_>), dim3((unsigned)grid), dim3(kThreads * RG_), 0, \
                      stream, B, nv, offsets, s, row_bytes, coeff, out, D, vec_out, d_status)
     if (bf16) {
       if (rg == 1) PAIR_MEAN(true, 1); else if (rg == 2) PAIR_MEAN(true, 2); else PAIR_MEAN(true, 4);
     } else {
-      if (rg == 1) PAIR_MEAN(false, 1); else if (rg == 2) PAIR_MEAN(false, 2); else PAIR_MEAN(false, 4);
+      if (rg == 1) PAIR_MEAN(false, 1); else PAIR_MEAN(false, 2);
     }
 #undef PAIR_MEAN
     return hipGetLastError() == hipSuccess ? PAIR_OK : PAIR_EHIP;
