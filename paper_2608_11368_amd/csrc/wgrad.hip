@@ -191,7 +191,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_kernel(
 // part q with kMeanBatch rows in flight per lane and the next batch's loads
 // issued before the current batch's FMAs.  The groups' partial sums are added
 // in LDS in group order at the end, so the result is deterministic for a
-// given D (RG depends only on D).  Workgroup 0 also checks that the offsets
+// given D and score type (RG depends only on them).  Workgroup 0 also checks that the offsets
 // are monotone.
 constexpr int kMeanBatch = 8;
 constexpr int kMeanChunk = 2048;
