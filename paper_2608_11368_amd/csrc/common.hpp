@@ -84,26 +84,29 @@ __device__ __forceinline__ float bf16lo_to_f32(uint32_t pair) { return __uint_as
 __device__ __forceinline__ float bf16hi_to_f32(uint32_t pair) {
   return __uint_as_float(pair & 0xffff0000u);
 }
-// Round-to-nearest-even fp32 -> bf16 (finite inputs; NaN kept quiet).
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
 // Value of `v` in lane `j` for a wave-uniform j (a scalar read of one lane,
 // no LDS round trip).
 __device__ __forceinline__ float lane_value(float v, int j) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), j));
 }
 
-// Butterfly sum across the 64 lanes: every lane ends with the same bits
-// (IEEE addition is commutative, so partner lanes form identical sums).
+// DPP move of a float within each row of 16 lanes.
+template <int kCtrl>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kCtrl, 0xf, 0xf, false));
+}
+
+// Sum across the 64 lanes, the same bits in every lane: four DPP steps
+// (quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror, row_mirror)
+// leave each row's total in all its lanes (partner lanes add the same two
+// values, and IEEE addition is commutative), then the four row totals are
+// added in row order.  Every lane of the wave must be active.
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) v += __shfl_xor(v, m, kWave);
-  return v;
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  v += dpp_f<0x141>(v);
+  v += dpp_f<0x140>(v);
+  return ((lane_value(v, 0) + lane_value(v, 16)) + lane_value(v, 32)) + lane_value(v, 48);
 }
 
 __device__ __forceinline__ void raise_status(int32_t* d_status, int32_t bits) {
