@@ -278,7 +278,8 @@ __global__ __launch_bounds__(kCoefThreads) void audit_coeffs_kernel(
       *reinterpret_cast<float4*>(drow + i0) = make_float4(d[i0], d[i0 + 1], d[i0 + 2], d[i0 + 3]);
   }
 
-  // Fixed-order column sums: butterfly within each wave, then waves in order.
+  // Fixed-order column sums: a wave sum (DPP steps within rows of 16 lanes,
+  // then the four rows in order) in each wave, then the waves in order.
 #pragma unroll
   for (int i = 0; i < KP; ++i) {
     const float sw = wave_sum(d[i]);
