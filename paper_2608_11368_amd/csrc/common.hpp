@@ -21,6 +21,21 @@ struct Philox4x64 {
   uint64_t w[4];
 };
 
+// Full 128-bit product m * c from four 32 x 32 -> 64-bit partial products,
+// the high and low halves sharing them: p01 and p10 carry the middle column,
+// and no sum can overflow 64 bits (each is at most (2^32 - 1)^2 plus two
+// 32-bit values).  Exact; four multiply-adds against about six for a
+// separate high product and low product.
+__device__ __forceinline__ void mulhilo64(uint64_t m, uint64_t c, uint64_t* hi, uint64_t* lo) {
+  const uint32_t c0 = (uint32_t)c, c1 = (uint32_t)(c >> 32);
+  const uint32_t m0 = (uint32_t)m, m1 = (uint32_t)(m >> 32);
+  const uint64_t p00 = (uint64_t)c0 * m0;
+  const uint64_t p01 = (uint64_t)c0 * m1 + (p00 >> 32);
+  const uint64_t p10 = (uint64_t)c1 * m0 + (uint32_t)p01;
+  *hi = (uint64_t)c1 * m1 + (p01 >> 32) + (p10 >> 32);
+  *lo = (p10 << 32) | (uint32_t)p00;
+}
+
 __device__ __forceinline__ Philox4x64 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2,
                                                     uint64_t c3, uint64_t k0, uint64_t k1) {
   const uint64_t m0 = 0xD2E7470EE14C6C93ull, m1 = 0xCA5A826395121157ull;
@@ -31,8 +46,9 @@ __device__ __forceinline__ Philox4x64 philox4x64_10(uint64_t c0, uint64_t c1, ui
       k0 += w0;
       k1 += w1;
     }
-    const uint64_t hi0 = __umul64hi(m0, c0), lo0 = m0 * c0;
-    const uint64_t hi1 = __umul64hi(m1, c2), lo1 = m1 * c2;
+    uint64_t hi0, lo0, hi1, lo1;
+    mulhilo64(m0, c0, &hi0, &lo0);
+    mulhilo64(m1, c2, &hi1, &lo1);
     const uint64_t n0 = hi1 ^ c1 ^ k0;
     const uint64_t n2 = hi0 ^ c3 ^ k1;
     c0 = n0;
